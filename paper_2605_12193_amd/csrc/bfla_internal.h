@@ -1,0 +1,60 @@
+// Host-side launcher interface between the C ABI (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "bfla_device.h"
+
+namespace bfla {
+
+struct PrefillLaunch {
+  const void* q;
+  void* o;
+  float* lse;
+  const int32_t* row_ptr;  // null -> dense (every causal tile)
+  const int32_t* cols;
+  int64_t q_sh, q_st, o_sh, o_st;
+  KvAddr kv;
+  int32_t h_q, h_kv, head_dim;
+  float scale;
+  Batch batch;  // requests in launch order (longest first)
+};
+
+bool prefill_supported(int head_dim, int m);
+hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream);
+
+struct ExpandLaunch {
+  const uint8_t* block_mask;
+  int32_t* row_ptr;
+  int32_t* cols;
+  int32_t* counts;   // workspace [n_rows]
+  int32_t* partial;  // workspace [scan blocks]
+  int32_t n_rows;
+  int32_t h_kv;
+  int32_t rb;        // b / T
+  int32_t n_local, n_sink, eta;
+  uint32_t rho24;    // floor(rho * 2^24); 1<<24 means every dropped tile
+  uint64_t seed;
+  Batch batch;       // requests in request order
+};
+
+hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream);
+size_t expand_workspace_bytes(int64_t n_rows);
+
+struct EstimateLaunch {
+  const void* q;
+  int64_t q_sh, q_st;
+  KvAddr kv;
+  uint8_t* block_mask;
+  float* scores;      // [per request H_q x L_q x L_kv], workspace or dbg output
+  int32_t h_q, h_kv, head_dim;
+  int32_t block, group;
+  float gamma;
+  float alpha;
+  Batch batch;        // requests in request order
+};
+
+bool estimate_supported(int head_dim, int block, int group);
+hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream);
+
+}  // namespace bfla

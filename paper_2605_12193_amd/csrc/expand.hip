@@ -1,0 +1,179 @@
+// Stage 2 tile mask and list compaction (eq19-eq26), integer only.
+//
+// One wave per list row (request, KV head, q-tile).  Lanes walk the causal
+// KV tiles of the row 64 at a time; each decides keep / drop for its tile:
+//   kept    = block mask of (qt / rb, kt / rb)          (eq20)
+//           | local band kt in [kt_diag - n_local, kt_diag]   (eq21)
+//           | sink kt < n_sink                            (eq22)
+//   rescued = !kept & (chi(qt, kt; s) mod eta == 0        (eq24)
+//                      | psi(h, qt, kt; s) < rho)         (eq25)
+// and the wave ballot gives counts (pass 1) or list positions (pass 3).
+// Pass 2 is an exclusive scan of the row counts in one workgroup.
+#include "bfla_device.h"
+#include "bfla_internal.h"
+
+namespace bfla {
+namespace {
+
+constexpr int TILE = 64;
+constexpr int ROWS_PER_WG = 4;
+constexpr int SCAN_THREADS = 1024;
+
+struct ExpandArgs {
+  const uint8_t* block_mask;
+  int32_t* row_ptr;
+  int32_t* cols;
+  int32_t* counts;
+  int32_t n_rows;
+  int32_t h_kv, rb;
+  int32_t n_local, n_sink, eta;
+  uint32_t rho24;
+  uint64_t chi_key;  // mix64(s)
+  uint64_t psi_key;  // mix64(s + 1)
+  Batch batch;
+};
+
+// SplitMix64 output mix (Steele, Lea and Flood, OOPSLA 2014).
+__host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+struct RowCtx {
+  const uint8_t* blk_row;  // block mask row of this q-tile's query block
+  int h, qt, kt_diag, n_tiles;
+};
+
+__device__ __forceinline__ bool row_ctx(const ExpandArgs& a, int row, RowCtx* c) {
+  if (row >= a.n_rows) return false;
+  int ri = 0;
+  for (int i = 1; i < a.batch.n_req; ++i)
+    if (row >= a.batch.r[i].row_base) ri = i;
+  const ReqDesc& R = a.batch.r[ri];
+  int local = row - R.row_base;
+  c->h = local / R.t_q;
+  c->qt = local % R.t_q;
+  int n_c = R.n_kv - R.n_q;
+  int last = min(n_c + (c->qt + 1) * TILE - 1, R.n_kv - 1);
+  c->kt_diag = last / TILE;
+  c->n_tiles = c->kt_diag + 1;
+  c->blk_row = a.block_mask + R.mask_off +
+               ((int64_t)c->h * R.l_q + c->qt / a.rb) * R.l_kv;
+  return true;
+}
+
+__device__ __forceinline__ bool keep_tile(const ExpandArgs& a, const RowCtx& c, int kt) {
+  if (kt > c.kt_diag) return false;
+  bool kept = c.blk_row[kt / a.rb] != 0;
+  kept |= (a.n_local >= 0) && (kt >= c.kt_diag - a.n_local);
+  kept |= kt < a.n_sink;
+  if (kept) return true;
+  const uint64_t key = ((uint64_t)c.qt << 21) | (uint64_t)kt;
+  if (a.eta > 0 && (mix64(a.chi_key ^ key) % (uint64_t)a.eta) == 0) return true;
+  if (a.rho24 > 0) {
+    uint64_t hk = key | ((uint64_t)(c.h + 1) << 42);
+    if ((uint32_t)(mix64(a.psi_key ^ hk) >> 40) < a.rho24) return true;
+  }
+  return false;
+}
+
+__global__ void __launch_bounds__(64 * ROWS_PER_WG) count_kernel(ExpandArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
+  RowCtx c;
+  if (!row_ctx(a, row, &c)) return;
+  int total = 0;
+  for (int k0 = 0; k0 < c.n_tiles; k0 += 64) {
+    unsigned long long b = __ballot(keep_tile(a, c, k0 + lane));
+    total += __popcll(b);
+  }
+  if (lane == 0) a.counts[row] = total;
+}
+
+__global__ void __launch_bounds__(SCAN_THREADS) scan_kernel(const int32_t* counts,
+                                                            int32_t* row_ptr, int n) {
+  __shared__ int32_t wsum[SCAN_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (n + SCAN_THREADS - 1) / SCAN_THREADS;
+  const int beg = min(n, tid * per), end = min(n, beg + per);
+  int s = 0;
+  for (int i = beg; i < end; ++i) s += counts[i];
+  // inclusive scan of s across the workgroup
+  int x = s;
+  for (int d = 1; d < 64; d <<= 1) {
+    int y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  if (wave == 0) {
+    int v = lane < SCAN_THREADS / 64 ? wsum[lane] : 0;
+    for (int d = 1; d < 64; d <<= 1) {
+      int y = __shfl_up(v, d);
+      if (lane >= d) v += y;
+    }
+    if (lane < SCAN_THREADS / 64) wsum[lane] = v;
+  }
+  __syncthreads();
+  int excl = x - s + (wave > 0 ? wsum[wave - 1] : 0);
+  for (int i = beg; i < end; ++i) {
+    row_ptr[i] = excl;
+    excl += counts[i];
+  }
+  if (tid == SCAN_THREADS - 1) row_ptr[n] = wsum[SCAN_THREADS / 64 - 1];
+}
+
+__global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
+  RowCtx c;
+  if (!row_ctx(a, row, &c)) return;
+  int pos = a.row_ptr[row];
+  for (int k0 = 0; k0 < c.n_tiles; k0 += 64) {
+    const int kt = k0 + lane;
+    const bool keep = keep_tile(a, c, kt);
+    unsigned long long b = __ballot(keep);
+    int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
+                                           __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0));
+    if (keep) a.cols[pos + before] = kt;
+    pos += __popcll(b);
+  }
+}
+
+}  // namespace
+
+size_t expand_workspace_bytes(int64_t n_rows) {
+  return (size_t)(((n_rows + 63) / 64) * 64 + 64) * sizeof(int32_t);
+}
+
+hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
+  if (L.n_rows == 0) return hipSuccess;
+  ExpandArgs a;
+  a.block_mask = L.block_mask;
+  a.row_ptr = L.row_ptr;
+  a.cols = L.cols;
+  a.counts = L.counts;
+  a.n_rows = L.n_rows;
+  a.h_kv = L.h_kv;
+  a.rb = L.rb;
+  a.n_local = L.n_local;
+  a.n_sink = L.n_sink;
+  a.eta = L.eta;
+  a.rho24 = L.rho24;
+  a.chi_key = mix64(L.seed);
+  a.psi_key = mix64(L.seed + 1);
+  a.batch = L.batch;
+  const int grid = (L.n_rows + ROWS_PER_WG - 1) / ROWS_PER_WG;
+  hipLaunchKernelGGL(count_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, stream, a.counts, a.row_ptr,
+                     a.n_rows);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace bfla

@@ -1,0 +1,141 @@
+"""The C-ABI library: it loads, exports every declared symbol, and rejects bad
+arguments before touching the GPU (these calls launch nothing)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2605_12193_amd import bfla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bfla.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(bfla._LIB_PATH),
+                                reason="libbfla.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(bfla_\w+)\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == set(bfla.EXPORTS)
+    lib = C.CDLL(bfla._LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings():
+    assert bfla.bfla_version() == "0.1.0"
+    assert bfla.bfla_status_string(0) == "ok"
+    assert bfla.bfla_status_string(4) == "list capacity too small"
+
+
+def _prob(n=(256,), h_q=4, h_kv=2, c=64):
+    return bfla.Problem(n, n, h_q, h_kv, c)
+
+
+def test_capacity_and_workspace_sizes():
+    p = _prob((256, 300))
+    prm = bfla.params()
+    cap = bfla.bfla_list_capacity(p, prm)
+    # rows: H_kv * T_q per request; causal tiles: T(T+1)/2 per head
+    assert cap.n_rows == 2 * 4 + 2 * 5
+    assert cap.max_cols == 2 * (4 * 5 // 2) + 2 * (5 * 6 // 2)
+    assert cap.mask_bytes == 2 * 2 * 2 + 2 * 3 * 3
+    assert cap.score_elems == 4 * 2 * 2 + 4 * 3 * 3
+    assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE) == cap.score_elems * 4
+    assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) >= cap.n_rows * 4
+    chunk = bfla.Problem([64], [320], 4, 2, 64)
+    cap2 = bfla.bfla_list_capacity(chunk, prm)
+    assert cap2.max_cols == 2 * 5          # one q-tile sees all 5 KV tiles
+
+
+@pytest.mark.parametrize("mut,status", [
+    (lambda p, q: setattr(p.c, "h_q", 5), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(p.c, "head_dim", 96), bfla.BFLA_ERR_UNSUPPORTED),
+    (lambda p, q: setattr(p.c, "batch", 0), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(p.c, "batch", 33), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "gamma", 0.0), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "gamma", 1.5), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "gamma", float("nan")), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "n_local", -2), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "n_sink", -1), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "eta", -1), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "rho", 1.5), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "tile", 32), bfla.BFLA_ERR_UNSUPPORTED),
+    (lambda p, q: setattr(q, "block", 96), bfla.BFLA_ERR_UNSUPPORTED),
+    (lambda p, q: setattr(q, "group", 48), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(q, "scale", -1.0), bfla.BFLA_ERR_INVALID_ARG),
+])
+def test_problem_and_param_errors(mut, status):
+    p, prm = _prob(), bfla.params()
+    mut(p, prm)
+    with pytest.raises(bfla.BflaError) as e:
+        bfla.bfla_list_capacity(p, prm)
+    assert e.value.status == status
+    assert bfla.lib().bfla_last_error().decode() != ""
+
+
+def test_bad_request_lengths():
+    prm = bfla.params()
+    with pytest.raises(bfla.BflaError) as e:
+        bfla.bfla_list_capacity(bfla.Problem([300], [200], 4, 2, 64), prm)
+    assert e.value.status == bfla.BFLA_ERR_INVALID_ARG
+    with pytest.raises(bfla.BflaError):
+        bfla.bfla_list_capacity(bfla.Problem([0], [10], 4, 2, 64), prm)
+
+
+def _fake_views():
+    """Views over fake (never dereferenced) aligned addresses: every call
+    below fails validation before any launch."""
+    addr = 1 << 20
+    v = bfla.bfla_view(addr, None, 0, 256 * 64, 64)
+    kv = bfla.bfla_kv(bfla.BFLA_KV_CONTIGUOUS, addr, addr, None, 0, 256 * 64, 64, 0, 0, 0, None)
+    return v, kv
+
+
+def test_entry_points_reject_before_launch():
+    L = bfla.lib()
+    p, prm = _prob(), bfla.params()
+    v, kv = _fake_views()
+    addr = C.c_void_p(1 << 20)
+    # null block mask
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), None, None,
+                              addr, 1 << 30, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
+    # workspace too small and no dbg output
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, None,
+                              addr, 4, None)
+    assert st == bfla.BFLA_ERR_WORKSPACE
+    # list capacity too small
+    st = L.bfla_expand_rescue(C.byref(p.c), C.byref(prm), addr, addr, addr, 3, addr, 1 << 20,
+                              None)
+    assert st == bfla.BFLA_ERR_CAPACITY
+    # expand workspace too small
+    st = L.bfla_expand_rescue(C.byref(p.c), C.byref(prm), addr, addr, addr, 1 << 20, addr, 0,
+                              None)
+    assert st == bfla.BFLA_ERR_WORKSPACE
+    # misaligned q
+    bad = bfla.bfla_view((1 << 20) + 2, None, 0, 256 * 64, 64)
+    st = L.bfla_sparse_prefill(C.byref(p.c), C.byref(prm), C.byref(bad), C.byref(kv), addr,
+                               addr, C.byref(v), None, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
+    # null lists
+    st = L.bfla_sparse_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), None,
+                               None, C.byref(v), None, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
+    # unsupported GQA group size 3
+    p3 = bfla.Problem([256], [256], 6, 2, 64)
+    st = L.bfla_dense_prefill(C.byref(p3.c), C.byref(prm), C.byref(v), C.byref(kv),
+                              C.byref(v), None, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
+    # paged K/V with too few pages in the table
+    pk = bfla.bfla_kv(bfla.BFLA_KV_PAGED, 1 << 20, 1 << 20, None, 0, 64, 128, 16, 8, 16 * 128,
+                      1 << 20)
+    st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
+                              None, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
