@@ -141,6 +141,11 @@ int check_kv(const bfla_problem* prob, const bfla_kv* kv, bool need_v) {
     return fail(BFLA_ERR_INVALID_ARG, "kv strides must be positive multiples of 8");
   if (kv->layout == BFLA_KV_CONTIGUOUS) {
     if (kv->stride_batch % 8) return fail(BFLA_ERR_INVALID_ARG, "kv stride_batch % 8 != 0");
+    // one KV head of one request is read through a buffer descriptor whose
+    // byte range is a signed 32-bit count
+    for (int r = 0; r < prob->batch; ++r)
+      if ((int64_t)(prob->n_kv[r] - 1) * kv->stride_tok + prob->head_dim >= (int64_t(1) << 30))
+        return fail(BFLA_ERR_UNSUPPORTED, "request %d: one KV head spans >= 2 GiB", r);
     if (kv->batch_offset)
       for (int r = 0; r < prob->batch; ++r)
         if (kv->batch_offset[r] < 0 || kv->batch_offset[r] % 8)

@@ -17,7 +17,14 @@
 //   chunk permuted (bits 2 and 3 of the key offset swapped) so that the
 //   accumulator's key order and the A operand's agree.
 // K/V tiles are double-buffered: the next list entry's tile is fetched into
-// registers while the current one is consumed from LDS.
+// registers while the current one is consumed from LDS.  Contiguous K/V are
+// read through buffer descriptors whose range check returns zeros past the
+// last key, so loads carry no branches.
+//
+// The online softmax keeps a stale running max: O and l are rescaled only
+// when a row's max grows by more than 2^RESCALE_LOG2 in the exp2 domain.
+// Both are always scaled by the same max, so O / l is exact, and every
+// weight stays <= 2^RESCALE_LOG2.
 #include "bfla_device.h"
 #include "bfla_internal.h"
 
@@ -26,6 +33,9 @@ namespace {
 
 constexpr int TILE = 64;
 constexpr float LOG2E = 1.4426950408889634f;
+constexpr float RESCALE_LOG2 = 8.0f;
+constexpr uint32_t RSRC_WORD3 = 0x00020000u;  // raw buffer, 32-bit data format
+constexpr int VMCNT0 = 0x0F70;                // s_waitcnt vmcnt(0), other counters free
 
 template <int C>
 struct Cfg {
@@ -43,7 +53,7 @@ struct PrefillArgs {
   const bf16_t* q;
   bf16_t* o;
   float* lse;
-  const int32_t* row_ptr;  // null -> dense
+  const int32_t* row_ptr;  // sparse lists (unused when dense)
   const int32_t* cols;
   int64_t q_sh, q_st, o_sh, o_st;
   KvAddr kv;
@@ -51,6 +61,9 @@ struct PrefillArgs {
   float scale;
   Batch batch;
 };
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -60,19 +73,12 @@ __device__ __forceinline__ uint4 ld16(const bf16_t* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) {
-  return __builtin_bit_cast(bf16x8, v);
-}
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// Round-to-nearest-even float -> bf16 bits (inputs here are finite or 0).
-__device__ __forceinline__ uint32_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
+// Two floats -> two bf16 (round to nearest even) in one word.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f2bf(lo) | (f2bf(hi) << 16);
+  f32x2 x = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
 }
 
 // Position of key offset k (0..63) inside the permuted V^T row.
@@ -80,7 +86,24 @@ __device__ __forceinline__ int vperm(int k) {
   return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
 }
 
-template <int C, int M>
+// Uniform reads of the tile lists through the constant address space, so
+// they become scalar loads (a vector load would be waited on together with the
+// in-flight K/V prefetch).
+typedef const __attribute__((address_space(4))) int32_t* const_i32_ptr;
+__device__ __forceinline__ int uniform_load(const int32_t* p, int i) {
+  return ((const_i32_ptr)p)[i];
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           (int)RSRC_WORD3);
+}
+
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
+template <int C, int M, bool DENSE, bool PAGED>
 __global__ void __launch_bounds__(128 * M)
 prefill_kernel(PrefillArgs a) {
   using CF = Cfg<C>;
@@ -101,103 +124,146 @@ prefill_kernel(PrefillArgs a) {
   // ---- work item -> (request, kv head, q-tile), longest rows first ----
   const int w = blockIdx.x;
   const int ri = find_req(a.batch, w);
-  const ReqDesc& R = a.batch.r[ri];
-  const int local = w - R.work_begin;
+  const ReqDesc& Rd = a.batch.r[ri];
+  const int n_q = Rd.n_q, n_kv = Rd.n_kv, t_q = Rd.t_q, t_kv = Rd.t_kv;
+  const int64_t q_off = Rd.q_off, o_off = Rd.o_off, kv_off = Rd.kv_off, lse_off = Rd.lse_off;
+  const int bt_row = Rd.bt_row;
+  const int local = w - Rd.work_begin;
+  const int row = Rd.row_base + (local % a.h_kv) * t_q + (t_q - 1 - local / a.h_kv);
   const int h = local % a.h_kv;
-  const int qt = R.t_q - 1 - local / a.h_kv;
-  const int n_c = R.n_kv - R.n_q;
-  const int row = R.row_base + h * R.t_q + qt;
+  const int qt = t_q - 1 - local / a.h_kv;
+  const int n_c = n_kv - n_q;
 
-  int list_begin, list_end;
-  if (a.row_ptr) {
-    list_begin = a.row_ptr[row];
-    list_end = a.row_ptr[row + 1];
+  int list_begin = 0, n_tiles;
+  if (DENSE) {
+    n_tiles = min(n_c + (qt + 1) * TILE - 1, n_kv - 1) / TILE + 1;
   } else {
-    int last = min(n_c + (qt + 1) * TILE - 1, R.n_kv - 1);
-    list_begin = 0;
-    list_end = last / TILE + 1;
+    list_begin = uniform_load(a.row_ptr, row);
+    n_tiles = uniform_load(a.row_ptr, row + 1) - list_begin;
   }
-  const int n_tiles = list_end - list_begin;
 
   // ---- this wave's queries ----
   const int p = h * a.m + (wave >> 1);
   const int t = qt * TILE + (wave & 1) * 32 + l32;   // query index in request
-  const bool q_ok = t < R.n_q;
+  const bool q_ok = t < n_q;
   const int q_pos = n_c + t;                          // absolute position
   const int wave_q0 = n_c + qt * TILE + (wave & 1) * 32;
+  const int key_lim = min(q_pos, n_kv - 1);           // last admissible key
 
   bf16x8 qf[NKC];
   {
-    const bf16_t* qp = a.q + R.q_off + (int64_t)p * a.q_sh + (int64_t)t * a.q_st + 8 * hi;
+    const bf16_t* qp = a.q + q_off + (int64_t)p * a.q_sh + (int64_t)t * a.q_st + 8 * hi;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
       uint4 v = q_ok ? ld16(qp + 16 * kc) : make_uint4(0, 0, 0, 0);
       qf[kc] = as_bf16x8(v);
     }
   }
+  // Q must be resident before the loop: otherwise the waitcnt pass keeps the
+  // Q loads pending at the loop header and waits for every outstanding load
+  // (including the next tile's prefetch) on each iteration.
+  __builtin_amdgcn_s_waitcnt(VMCNT0);
 
-  // ---- tile staging (global -> registers -> LDS) ----
+  // ---- K/V addressing ----
+  const int64_t st = a.kv.stride_tok;
+  __amdgpu_buffer_rsrc_t krs, vrs;
+  if (!PAGED) {
+    const int64_t head_off = kv_off + (int64_t)h * a.kv.stride_head;
+    const uint32_t bytes = (uint32_t)(((int64_t)(n_kv - 1) * st + C) * 2);
+    krs = make_rsrc(a.kv.k + head_off, bytes);
+    vrs = make_rsrc(a.kv.v + head_off, bytes);
+  }
+  // per-thread constant parts of the staging pattern
+  int k_row[KC_PER_T], k_ce[KC_PER_T];
+  uint32_t k_boff[KC_PER_T];  // byte offset inside a contiguous tile
+#pragma unroll
+  for (int i = 0; i < KC_PER_T; ++i) {
+    int e = tid + i * NT;
+    k_row[i] = e / (C / 8);
+    k_ce[i] = e % (C / 8);
+    k_boff[i] = (uint32_t)(((int64_t)k_row[i] * st + 8 * k_ce[i]) * 2);
+  }
+  int v_j[VU_PER_T], v_ce[VU_PER_T];
+  uint32_t v_boff[VU_PER_T];
+#pragma unroll
+  for (int i = 0; i < VU_PER_T; ++i) {
+    int u = tid + i * NT;
+    v_j[i] = u / (C / 8);
+    v_ce[i] = u % (C / 8);
+    v_boff[i] = (uint32_t)(((int64_t)(2 * v_j[i]) * st + 8 * v_ce[i]) * 2);
+  }
+  const uint32_t tile_bytes = (uint32_t)(TILE * st * 2);
+  const uint32_t st_bytes = (uint32_t)(st * 2);
+
   uint4 kreg[KC_PER_T];
   uint4 vreg[VU_PER_T][2];
 
-  auto tile_of = [&](int i) -> int {
-    return a.row_ptr ? a.cols[list_begin + i] : i;
+  auto paged_elem = [&](int key) -> int64_t {
+    int page = a.kv.block_table[(int64_t)bt_row * a.kv.max_pages + key / a.kv.page_size];
+    return (int64_t)page * a.kv.page_stride + (int64_t)(key % a.kv.page_size) * st +
+           (int64_t)h * a.kv.stride_head;
   };
 
   auto load_tile = [&](int kt) {
+    // tiles outside [0, T_kv) (malformed lists) load nothing
+    const bool ok = (unsigned)kt < (unsigned)t_kv;
+    if (!PAGED) {
+      // past-the-end offsets (and 2^31 for a bad tile) read as zeros
+      const uint32_t base = ok ? (uint32_t)kt * tile_bytes : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i)
+        if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+          kreg[i] = bload16(krs, base + k_boff[i]);
+#pragma unroll
+      for (int i = 0; i < VU_PER_T; ++i)
+        if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+          vreg[i][0] = bload16(vrs, base + v_boff[i]);
+          vreg[i][1] = bload16(vrs, base + v_boff[i] + st_bytes);
+        }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i) {
-      int e = tid + i * NT;
       kreg[i] = make_uint4(0, 0, 0, 0);
-      if (e < CF::K_CHUNKS) {
-        int kr = e / (C / 8), ce = e % (C / 8);
-        int key = kt * TILE + kr;
-        if ((unsigned)key < (unsigned)R.n_kv)
-          kreg[i] = ld16(a.kv.k + kv_elem(a.kv, R, h, key) + 8 * ce);
+      if ((CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS) && ok) {
+        const int key = kt * TILE + k_row[i];
+        if (key < n_kv) kreg[i] = ld16(a.kv.k + paged_elem(key) + 8 * k_ce[i]);
       }
     }
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i) {
-      int u = tid + i * NT;
       vreg[i][0] = make_uint4(0, 0, 0, 0);
       vreg[i][1] = make_uint4(0, 0, 0, 0);
-      if (u < CF::V_UNITS) {
-        int ce = u % (C / 8), j = u / (C / 8);
-        int key = kt * TILE + 2 * j;
-        if ((unsigned)key < (unsigned)R.n_kv)
-          vreg[i][0] = ld16(a.kv.v + kv_elem(a.kv, R, h, key) + 8 * ce);
-        if ((unsigned)(key + 1) < (unsigned)R.n_kv)
-          vreg[i][1] = ld16(a.kv.v + kv_elem(a.kv, R, h, key + 1) + 8 * ce);
+      if ((CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) && ok) {
+        const int key = kt * TILE + 2 * v_j[i];
+        if (key < n_kv) vreg[i][0] = ld16(a.kv.v + paged_elem(key) + 8 * v_ce[i]);
+        if (key + 1 < n_kv) vreg[i][1] = ld16(a.kv.v + paged_elem(key + 1) + 8 * v_ce[i]);
       }
     }
   };
 
-  auto store_tile = [&](bf16_t* st) {
-    bf16_t* ks = st;
-    bf16_t* vs = st + CF::K_ELEMS;
+  auto store_tile = [&](bf16_t* stg) {
+    bf16_t* ks = stg;
+    bf16_t* vs = stg + CF::K_ELEMS;
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i) {
-      int e = tid + i * NT;
-      if (e < CF::K_CHUNKS) {
-        int kr = e / (C / 8), ce = e % (C / 8);
-        *reinterpret_cast<uint4*>(ks + kr * CF::KROW + 8 * ce) = kreg[i];
-      }
+      if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+        *reinterpret_cast<uint4*>(ks + k_row[i] * CF::KROW + 8 * k_ce[i]) = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i) {
-      int u = tid + i * NT;
-      if (u < CF::V_UNITS) {
-        int ce = u % (C / 8), j = u / (C / 8);
-        int pos = vperm(2 * j);
+      if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+        const int pos = vperm(2 * v_j[i]);
         const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
         const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+        bf16_t* col = vs + 8 * v_ce[i] * CF::VROW + pos;
 #pragma unroll
         for (int e2 = 0; e2 < 4; ++e2) {
           // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
-          uint32_t lo = (r0[e2] & 0xFFFFu) | (r1[e2] << 16);
-          uint32_t hi2 = (r0[e2] >> 16) | (r1[e2] & 0xFFFF0000u);
-          *reinterpret_cast<uint32_t*>(vs + (8 * ce + 2 * e2) * CF::VROW + pos) = lo;
-          *reinterpret_cast<uint32_t*>(vs + (8 * ce + 2 * e2 + 1) * CF::VROW + pos) = hi2;
+          const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
+          const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
+          *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
+          *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
         }
       }
     }
@@ -205,7 +271,7 @@ prefill_kernel(PrefillArgs a) {
 
   // ---- online softmax state (one query per lane; both lane halves agree) ----
   const float c2 = a.scale * LOG2E;
-  float m_run = -INFINITY;
+  float m_run = -INFINITY;   // stale running max of the raw scores
   float l_run = 0.f;
   f32x16 acc[NCB];
 #pragma unroll
@@ -213,16 +279,26 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
+  auto tile_at = [&](int i) -> int { return DENSE ? i : uniform_load(a.cols, list_begin + i); };
+
+  int kt_next = 0;
   if (n_tiles > 0) {
-    load_tile(tile_of(0));
+    const int kt0 = tile_at(0);
+    load_tile(kt0);
     store_tile(lds);
+    if (n_tiles > 1) kt_next = tile_at(1);
   }
   __syncthreads();
 
+  int kt = n_tiles > 0 ? tile_at(0) : 0;
   for (int it = 0; it < n_tiles; ++it) {
-    const int kt = tile_of(it);
     const bool more = it + 1 < n_tiles;
-    if (more) load_tile(tile_of(it + 1));
+    const int kt_cur = kt;
+    if (more) {
+      load_tile(kt_next);
+      kt = kt_next;
+      if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
+    }
 
     const bf16_t* ks = lds + (it & 1) * CF::STAGE;
     const bf16_t* vs = ks + CF::K_ELEMS;
@@ -239,17 +315,16 @@ prefill_kernel(PrefillArgs a) {
       s1 = mfma32(a1, qf[kc], s1);
     }
 
-    // token-level causal mask and key bound, only where the tile needs it;
-    // a list entry outside [0, T_kv) contributes nothing
-    const int key0 = kt * TILE;
-    if ((unsigned)kt >= (unsigned)R.t_kv || key0 + TILE - 1 > wave_q0 || key0 + TILE > R.n_kv) {
-      const bool bad = (unsigned)kt >= (unsigned)R.t_kv;
+    // token-level causal mask and key bound, only on tiles that need it; a
+    // list entry outside [0, T_kv) contributes nothing
+    const int key0 = kt_cur * TILE;
+    if ((unsigned)kt_cur >= (unsigned)t_kv || key0 + TILE - 1 > wave_q0 || key0 + TILE > n_kv) {
+      const int lim = ((unsigned)kt_cur >= (unsigned)t_kv ? -1 : key_lim) - key0 - 4 * hi;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        int kk = key0 + 8 * (r >> 2) + 4 * hi + (r & 3);
-        if (bad || kk > q_pos || kk >= R.n_kv) s0[r] = -INFINITY;
-        kk += 32;
-        if (bad || kk > q_pos || kk >= R.n_kv) s1[r] = -INFINITY;
+        const int kk = 8 * (r >> 2) + (r & 3);
+        s0[r] = kk <= lim ? s0[r] : -INFINITY;
+        s1[r] = kk + 32 <= lim ? s1[r] : -INFINITY;
       }
     }
 
@@ -257,10 +332,19 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float corr = __builtin_amdgcn_exp2f((m_run - m_use) * c2);
-    const float moff = -m_use * c2;
+    // move the stale max only when the new max exceeds it by 2^RESCALE_LOG2
+    const bool grow = (mx - m_run) * c2 > RESCALE_LOG2 || (m_run == -INFINITY && mx != -INFINITY);
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      const float m_new = grow ? mx : m_run;
+      const float corr = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c2) : 1.f;
+      m_run = m_new;
+      l_run *= corr;
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[cb][r] *= corr;
+    }
+    const float moff = (m_run == -INFINITY) ? 0.f : -m_run * c2;
     float rs = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -269,12 +353,7 @@ prefill_kernel(PrefillArgs a) {
       rs += s0[r] + s1[r];
     }
     rs += __shfl_xor(rs, 32);
-    l_run = l_run * corr + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[cb][r] *= corr;
+    l_run += rs;
 
     // P^T (bf16) as B operands: 16-key chunk q = regs 8(q%2).. of block q/2
     bf16x8 pf[4];
@@ -307,7 +386,7 @@ prefill_kernel(PrefillArgs a) {
   // ---- epilogue: O = O^T / l, LSE ----
   if (!q_ok) return;
   const float inv = (l_run > 0.f) ? 1.f / l_run : 0.f;
-  bf16_t* op = a.o + R.o_off + (int64_t)p * a.o_sh + (int64_t)t * a.o_st;
+  bf16_t* op = a.o + o_off + (int64_t)p * a.o_sh + (int64_t)t * a.o_st;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
@@ -320,13 +399,13 @@ prefill_kernel(PrefillArgs a) {
   }
   if (a.lse && hi == 0) {
     float v = (l_run > 0.f) ? m_run * a.scale + logf(l_run) : -INFINITY;
-    a.lse[R.lse_off + (int64_t)p * R.n_q + t] = v;
+    a.lse[lse_off + (int64_t)p * n_q + t] = v;
   }
 }
 
-template <int C, int M>
-hipError_t launch_c_m(const PrefillArgs& a, int n_work, hipStream_t s) {
-  auto kern = prefill_kernel<C, M>;
+template <int C, int M, bool DENSE, bool PAGED>
+hipError_t launch_one(const PrefillArgs& a, int n_work, hipStream_t s) {
+  auto kern = prefill_kernel<C, M, DENSE, PAGED>;
   constexpr int lds = Cfg<C>::LDS_BYTES;
   static_assert(lds <= 160 * 1024, "LDS budget");
   static bool attr_set = false;  // idempotent; a benign race sets it twice
@@ -340,14 +419,23 @@ hipError_t launch_c_m(const PrefillArgs& a, int n_work, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int C, int M>
+hipError_t launch_c_m(const PrefillArgs& a, bool dense, int n_work, hipStream_t s) {
+  const bool paged = a.kv.paged != 0;
+  if (dense) return paged ? launch_one<C, M, true, true>(a, n_work, s)
+                          : launch_one<C, M, true, false>(a, n_work, s);
+  return paged ? launch_one<C, M, false, true>(a, n_work, s)
+               : launch_one<C, M, false, false>(a, n_work, s);
+}
+
 template <int C>
-hipError_t launch_c(const PrefillArgs& a, int n_work, hipStream_t s) {
+hipError_t launch_c(const PrefillArgs& a, bool dense, int n_work, hipStream_t s) {
   switch (a.m) {
-    case 1: return launch_c_m<C, 1>(a, n_work, s);
-    case 2: return launch_c_m<C, 2>(a, n_work, s);
-    case 4: return launch_c_m<C, 4>(a, n_work, s);
-    case 5: return launch_c_m<C, 5>(a, n_work, s);
-    case 8: return launch_c_m<C, 8>(a, n_work, s);
+    case 1: return launch_c_m<C, 1>(a, dense, n_work, s);
+    case 2: return launch_c_m<C, 2>(a, dense, n_work, s);
+    case 4: return launch_c_m<C, 4>(a, dense, n_work, s);
+    case 5: return launch_c_m<C, 5>(a, dense, n_work, s);
+    case 8: return launch_c_m<C, 8>(a, dense, n_work, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -383,10 +471,11 @@ hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
     n_work += a.h_kv * a.batch.r[i].t_q;
   }
   if (n_work == 0) return hipSuccess;
+  const bool dense = L.row_ptr == nullptr;
   switch (L.head_dim) {
-    case 64: return launch_c<64>(a, n_work, stream);
-    case 128: return launch_c<128>(a, n_work, stream);
-    case 256: return launch_c<256>(a, n_work, stream);
+    case 64: return launch_c<64>(a, dense, n_work, stream);
+    case 128: return launch_c<128>(a, dense, n_work, stream);
+    case 256: return launch_c<256>(a, dense, n_work, stream);
     default: return hipErrorInvalidValue;
   }
 }
