@@ -187,9 +187,11 @@ prefill_kernel(PrefillArgs a) {
   uint32_t v_boff[VU_PER_T];
 #pragma unroll
   for (int i = 0; i < VU_PER_T; ++i) {
+    // key pair fastest: the 16 lanes of one LDS store phase write 16
+    // consecutive words of one V^T row (distinct banks)
     int u = tid + i * NT;
-    v_j[i] = u / (C / 8);
-    v_ce[i] = u % (C / 8);
+    v_j[i] = u % (TILE / 2);
+    v_ce[i] = u / (TILE / 2);
     v_boff[i] = (uint32_t)(((int64_t)(2 * v_j[i]) * st + 8 * v_ce[i]) * 2);
   }
   const uint32_t tile_bytes = (uint32_t)(TILE * st * 2);
@@ -328,9 +330,10 @@ prefill_kernel(PrefillArgs a) {
       }
     }
 
-    float mx = -INFINITY;
+    // row max over this lane's 32 keys: a chain of 3-input max
+    float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    for (int r = 1; r < 16; ++r) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     // move the stale max only when the new max exceeds it by 2^RESCALE_LOG2
     const bool grow = (mx - m_run) * c2 > RESCALE_LOG2 || (m_run == -INFINITY && mx != -INFINITY);
@@ -345,13 +348,15 @@ prefill_kernel(PrefillArgs a) {
         for (int r = 0; r < 16; ++r) acc[cb][r] *= corr;
     }
     const float moff = (m_run == -INFINITY) ? 0.f : -m_run * c2;
-    float rs = 0.f;
+    float rs0 = 0.f, rs1 = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], c2, moff));
       s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], c2, moff));
-      rs += s0[r] + s1[r];
+      rs0 += s0[r];
+      rs1 += s1[r];
     }
+    float rs = rs0 + rs1;
     rs += __shfl_xor(rs, 32);
     l_run += rs;
 
