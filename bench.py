@@ -34,6 +34,33 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
+def prefill_source_hash() -> str:
+    import hashlib
+    m = hashlib.sha256()
+    for f in ("paper_2605_12193_amd/csrc/prefill.hip", "paper_2605_12193_amd/csrc/bfla_device.h"):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            m.update(fh.read())
+    return m.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per sparse-prefill launch from the committed rocprofv3 counter
+    summary, or None if there is none for this workload or the kernel source
+    changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "prefill_" + workload.replace("_", "") + "_traffic.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 2:
+            kv[parts[0]] = parts[1]
+    if kv.get("source_hash") != prefill_source_hash() or kv.get("workload") != workload:
+        return None
+    v = kv.get("traffic_bytes_prefill_sparse")
+    return float(v) if v else None
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -50,6 +77,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle sample")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, copy a buffer of this many MiB once (a dispatch "
+                         "of known HBM traffic for scaling FETCH_SIZE / WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -256,13 +286,22 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "prefill_kernel (sparse)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None,
+                     "traffic": measured_traffic(wl.name),
                      "flop_per_launch": flop_kept,
                      "launch_ms": round(float(pre_ms), 3)},
         "wall_s_timed": round(wall, 3),
         "input_gen_s": round(t_gen, 1),
     }
     log(f"dense {dense_ms:.3f} ms")
+    if args.calib_copy_mib > 0:
+        nbytes = args.calib_copy_mib << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
     if not args.no_cpu:
         gpu_o = o.float().cpu().numpy()
         cpu, err = cpu_baseline(wl, seq, gpu_o, args.cpu_seconds)

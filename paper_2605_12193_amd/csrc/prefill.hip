@@ -44,7 +44,9 @@ struct Cfg {
   static constexpr int K_ELEMS = TILE * KROW;
   static constexpr int V_ELEMS = C * VROW;
   static constexpr int STAGE = K_ELEMS + V_ELEMS;
-  static constexpr int LDS_BYTES = 2 * STAGE * 2;
+  // three stages (ping-pong schedule) when they fit the 160 KB of LDS
+  static constexpr bool PING_PONG = 3 * STAGE * 2 <= 160 * 1024;
+  static constexpr int LDS_BYTES = (PING_PONG ? 3 : 2) * STAGE * 2;
   static constexpr int K_CHUNKS = TILE * C / 8;   // 16-byte chunks per K tile
   static constexpr int V_UNITS = (TILE / 2) * (C / 8);  // key pairs x 8 channels
 };
@@ -103,10 +105,27 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off)
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
 
+// Scheduling pins for an MFMA stream fed from LDS: the first DEPTH operand
+// reads, then alternating (MFMA, read) pairs, then the last DEPTH MFMAs.
+// Without them the scheduler keeps only ~2 reads in flight and every MFMA
+// waits on the LDS latency.
+constexpr int SG_MFMA = 0x008, SG_DS_READ = 0x100;
+template <int DEPTH, int N>
+__device__ __forceinline__ void pin_read_ahead() {
+  __builtin_amdgcn_sched_group_barrier(SG_DS_READ, DEPTH, 0);
+#pragma unroll
+  for (int j = 0; j < N - DEPTH; ++j) {
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(SG_MFMA, DEPTH, 0);
+}
+
 template <int C, int M, bool DENSE, bool PAGED>
 __global__ void __launch_bounds__(128 * M)
 prefill_kernel(PrefillArgs a) {
   using CF = Cfg<C>;
+  constexpr bool PP = CF::PING_PONG && M >= 4;  // both groups need >= 4 waves
   constexpr int NT = 128 * M;
   constexpr int KC_PER_T = (CF::K_CHUNKS + NT - 1) / NT;
   constexpr int VU_PER_T = (CF::V_UNITS + NT - 1) / NT;
@@ -282,46 +301,39 @@ prefill_kernel(PrefillArgs a) {
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
   auto tile_at = [&](int i) -> int { return DENSE ? i : uniform_load(a.cols, list_begin + i); };
+  auto stage = [&](int slot) -> bf16_t* { return lds + slot * CF::STAGE; };
 
-  int kt_next = 0;
-  if (n_tiles > 0) {
-    const int kt0 = tile_at(0);
-    load_tile(kt0);
-    store_tile(lds);
-    if (n_tiles > 1) kt_next = tile_at(1);
-  }
-  __syncthreads();
-
-  int kt = n_tiles > 0 ? tile_at(0) : 0;
-  for (int it = 0; it < n_tiles; ++it) {
-    const bool more = it + 1 < n_tiles;
-    const int kt_cur = kt;
-    if (more) {
-      load_tile(kt_next);
-      kt = kt_next;
-      if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
-    }
-
-    const bf16_t* ks = lds + (it & 1) * CF::STAGE;
-    const bf16_t* vs = ks + CF::K_ELEMS;
-
-    // S^T = K . Q^T  (two 32-key blocks)
-    f32x16 s0, s1;
+  // S^T = K . Q^T  (two 32-key blocks) from the K tile of one stage.  The
+  // LDS operand reads run DEPTH fragments ahead of the MFMAs that use them.
+  constexpr int DEPTH = 4;
+  f32x16 s0, s1;
+  auto k_frag = [&](const bf16_t* ks, int j) -> bf16x8 {   // j = 2 kc + block
+    return as_bf16x8(ld16(ks + ((j & 1) * 32 + l32) * CF::KROW + 16 * (j >> 1) + 8 * hi));
+  };
+  auto qk = [&](const bf16_t* ks) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) { s0[r] = 0.f; s1[r] = 0.f; }
+    bf16x8 ring[DEPTH];
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
-      bf16x8 a0 = as_bf16x8(ld16(ks + l32 * CF::KROW + 16 * kc + 8 * hi));
-      bf16x8 a1 = as_bf16x8(ld16(ks + (32 + l32) * CF::KROW + 16 * kc + 8 * hi));
-      s0 = mfma32(a0, qf[kc], s0);
-      s1 = mfma32(a1, qf[kc], s1);
+    for (int j = 0; j < DEPTH; ++j) ring[j] = k_frag(ks, j);
+#pragma unroll
+    for (int j = 0; j < 2 * NKC; ++j) {
+      const bf16x8 a = ring[j % DEPTH];
+      if (j + DEPTH < 2 * NKC) ring[j % DEPTH] = k_frag(ks, j + DEPTH);
+      if (j & 1) s1 = mfma32(a, qf[j >> 1], s1);
+      else s0 = mfma32(a, qf[j >> 1], s0);
     }
+    pin_read_ahead<DEPTH, 2 * NKC>();
+  };
 
+  // online softmax of the scores of KV tile kt -> bf16 P^T operands
+  bf16x8 pf[4];
+  auto softmax = [&](int kt_s) {
     // token-level causal mask and key bound, only on tiles that need it; a
     // list entry outside [0, T_kv) contributes nothing
-    const int key0 = kt_cur * TILE;
-    if ((unsigned)kt_cur >= (unsigned)t_kv || key0 + TILE - 1 > wave_q0 || key0 + TILE > n_kv) {
-      const int lim = ((unsigned)kt_cur >= (unsigned)t_kv ? -1 : key_lim) - key0 - 4 * hi;
+    const int key0 = kt_s * TILE;
+    if ((unsigned)kt_s >= (unsigned)t_kv || key0 + TILE - 1 > wave_q0 || key0 + TILE > n_kv) {
+      const int lim = ((unsigned)kt_s >= (unsigned)t_kv ? -1 : key_lim) - key0 - 4 * hi;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int kk = 8 * (r >> 2) + (r & 3);
@@ -329,7 +341,6 @@ prefill_kernel(PrefillArgs a) {
         s1[r] = kk + 32 <= lim ? s1[r] : -INFINITY;
       }
     }
-
     // row max over this lane's 32 keys: a chain of 3-input max
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
@@ -359,9 +370,7 @@ prefill_kernel(PrefillArgs a) {
     float rs = rs0 + rs1;
     rs += __shfl_xor(rs, 32);
     l_run += rs;
-
     // P^T (bf16) as B operands: 16-key chunk q = regs 8(q%2).. of block q/2
-    bf16x8 pf[4];
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
       const f32x16& sb = (qq < 2) ? s0 : s1;
@@ -373,19 +382,104 @@ prefill_kernel(PrefillArgs a) {
       u.w = pack_bf16x2(sb[base + 6], sb[base + 7]);
       pf[qq] = as_bf16x8(u);
     }
+  };
 
-    // O^T += V^T . P^T
+  // O^T += V^T . P^T from the V^T tile of one stage (same read-ahead ring).
+  // The channel block varies fastest, so consecutive MFMAs accumulate into
+  // different registers.
+  auto v_frag = [&](const bf16_t* vs, int j) -> bf16x8 {   // j = NCB q + cb
+    return as_bf16x8(ld16(vs + (32 * (j % NCB) + l32) * CF::VROW + 16 * (j / NCB) + 8 * hi));
+  };
+  auto pv = [&](const bf16_t* vs) {
+    bf16x8 ring[DEPTH];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
+    for (int j = 0; j < DEPTH; ++j) ring[j] = v_frag(vs, j);
 #pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        bf16x8 av = as_bf16x8(ld16(vs + (32 * cb + l32) * CF::VROW + 16 * qq + 8 * hi));
-        acc[cb] = mfma32(av, pf[qq], acc[cb]);
-      }
+    for (int j = 0; j < 4 * NCB; ++j) {
+      const bf16x8 a = ring[j % DEPTH];
+      if (j + DEPTH < 4 * NCB) ring[j % DEPTH] = v_frag(vs, j + DEPTH);
+      acc[j % NCB] = mfma32(a, pf[j / NCB], acc[j % NCB]);
     }
+    pin_read_ahead<DEPTH, 4 * NCB>();
+  };
 
-    if (more) store_tile(lds + ((it + 1) & 1) * CF::STAGE);
+  if (PP) {
+    // Ping-pong over 3 LDS stages.  Group A (waves 0-3 of every 8) runs half
+    // an iteration ahead of group B (waves 4-7); each SIMD hosts one wave of
+    // each group, so in every phase one of them issues MFMAs while the other
+    // runs the softmax.  Tile i lives in stage i % 3.
+    //   phase X_i: A softmax(i)            | B PV(i-1), QK(i)
+    //   phase Y_i: A PV(i), QK(i+1)        | B softmax(i); all: store tile i+2
+    // Stage (i+2) % 3 == (i-1) % 3 is last read by B in phase X_i.
+    const bool grp_a = ((wave >> 2) & 1) == 0;
+    int kt_i = 0, kt_i1 = 0, kt_i2 = 0, kt_i3 = 0;  // tiles i .. i+3
+    if (n_tiles > 0) kt_i = tile_at(0);
+    if (n_tiles > 1) kt_i1 = tile_at(1);
+    if (n_tiles > 2) kt_i2 = tile_at(2);
+    if (n_tiles > 3) kt_i3 = tile_at(3);
+    if (n_tiles > 0) { load_tile(kt_i); store_tile(stage(0)); }
+    if (n_tiles > 1) { load_tile(kt_i1); store_tile(stage(1)); }
+    if (n_tiles > 2) load_tile(kt_i2);
     __syncthreads();
+    if (grp_a && n_tiles > 0) qk(stage(0));
+    __syncthreads();
+    int slot = 0;  // i % 3
+    for (int it = 0; it < n_tiles; ++it) {
+      const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
+      const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
+      // phase X
+      if (grp_a) {
+        softmax(kt_i);
+      } else {
+        if (it > 0) pv(stage(slot2) + CF::K_ELEMS);
+        qk(stage(slot));
+      }
+      __syncthreads();
+      // phase Y
+      if (grp_a) {
+        pv(stage(slot) + CF::K_ELEMS);
+        if (it + 1 < n_tiles) qk(stage(slot1));
+      } else {
+        softmax(kt_i);
+      }
+      if (it + 2 < n_tiles) {
+        store_tile(stage(slot2));
+        if (it + 3 < n_tiles) load_tile(kt_i3);
+      }
+      kt_i = kt_i1;
+      kt_i1 = kt_i2;
+      kt_i2 = kt_i3;
+      if (it + 4 < n_tiles) kt_i3 = tile_at(it + 4);
+      slot = slot1;
+      __syncthreads();
+    }
+    if (!grp_a && n_tiles > 0) pv(stage(slot == 0 ? 2 : slot - 1) + CF::K_ELEMS);
+  } else {
+    // Two LDS stages, every wave in the same phase: the next list entry's
+    // tile is fetched into registers while the current one is consumed.
+    int kt_next = 0;
+    if (n_tiles > 0) {
+      load_tile(tile_at(0));
+      store_tile(stage(0));
+      if (n_tiles > 1) kt_next = tile_at(1);
+    }
+    __syncthreads();
+    int kt = n_tiles > 0 ? tile_at(0) : 0;
+    for (int it = 0; it < n_tiles; ++it) {
+      const bool more = it + 1 < n_tiles;
+      const int kt_cur = kt;
+      if (more) {
+        load_tile(kt_next);
+        kt = kt_next;
+        if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
+      }
+      const bf16_t* ks = stage(it & 1);
+      qk(ks);
+      softmax(kt_cur);
+      pv(ks + CF::K_ELEMS);
+      if (more) store_tile(stage((it + 1) & 1));
+      __syncthreads();
+    }
   }
 
   // ---- epilogue: O = O^T / l, LSE ----
