@@ -92,11 +92,14 @@ enum { BFLA_KV_CONTIGUOUS = 0, BFLA_KV_PAGED = 1 };
 
 /* K and V (same layout, separate base pointers).
  * CONTIGUOUS: element (r, h, t, c) at  base + off(r) + h*stride_head +
- *             t*stride_tok + c, off(r) as in bfla_view.
+ *             t*stride_tok + c, off(r) as in bfla_view.  One KV head of one
+ *             request must span less than 2 GiB.
  * PAGED (vLLM-style): token t of request r lives in page
  *             P = block_table[r * max_pages + t / page_size]
  *             at  base + P*page_stride + (t % page_size)*stride_tok +
- *             h*stride_head + c. */
+ *             h*stride_head + c.  The pool holds n_pages pages and must be
+ *             smaller than 2 GiB; a table entry outside [0, n_pages) reads as
+ *             zeros (never out of bounds). */
 typedef struct bfla_kv {
   int32_t layout;               /* BFLA_KV_CONTIGUOUS or BFLA_KV_PAGED */
   const void* k;                /* device, bf16 */
@@ -105,10 +108,11 @@ typedef struct bfla_kv {
   int64_t stride_batch;         /* CONTIGUOUS */
   int64_t stride_head;
   int64_t stride_tok;
-  int32_t page_size;            /* PAGED: tokens per page, multiple of 16 */
+  int32_t page_size;            /* PAGED: tokens per page, a power of two >= 16 */
   int32_t max_pages;            /* PAGED: row length of block_table */
   int64_t page_stride;          /* PAGED: elements between pages */
   const int32_t* block_table;   /* PAGED: device [batch][max_pages] */
+  int64_t n_pages;              /* PAGED: pages in the pool */
 } bfla_kv;
 
 /* Method hyper-parameters. */

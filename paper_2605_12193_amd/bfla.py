@@ -41,7 +41,8 @@ class bfla_kv(C.Structure):
                 ("batch_offset", C.POINTER(C.c_int64)), ("stride_batch", C.c_int64),
                 ("stride_head", C.c_int64), ("stride_tok", C.c_int64),
                 ("page_size", C.c_int32), ("max_pages", C.c_int32),
-                ("page_stride", C.c_int64), ("block_table", C.c_void_p)]
+                ("page_stride", C.c_int64), ("block_table", C.c_void_p),
+                ("n_pages", C.c_int64)]
 
 
 class bfla_params(C.Structure):
@@ -174,7 +175,7 @@ class KV:
             # pools [pages][page_size][H_kv][C]
             self.c = bfla_kv(BFLA_KV_PAGED, k.data_ptr(), v.data_ptr(), None, 0,
                              k.stride(2), k.stride(1), k.shape[1], block_table.shape[1],
-                             k.stride(0), block_table.data_ptr())
+                             k.stride(0), block_table.data_ptr(), k.shape[0])
         else:
             if batch_offsets is not None:
                 self._off = (C.c_int64 * len(batch_offsets))(*batch_offsets)
@@ -183,7 +184,7 @@ class KV:
             else:              # [B][H][N][C]
                 sb, sh, st = k.stride(0), k.stride(1), k.stride(2)
             self.c = bfla_kv(BFLA_KV_CONTIGUOUS, k.data_ptr(), v.data_ptr(), self._off,
-                             sb, sh, st, 0, 0, 0, None)
+                             sb, sh, st, 0, 0, 0, None, 0)
 
 
 # ---------------------------------------------------------------------------

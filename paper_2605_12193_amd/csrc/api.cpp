@@ -151,7 +151,14 @@ int check_kv(const bfla_problem* prob, const bfla_kv* kv, bool need_v) {
         if (kv->batch_offset[r] < 0 || kv->batch_offset[r] % 8)
           return fail(BFLA_ERR_INVALID_ARG, "kv batch_offset[%d] invalid", r);
   } else if (kv->layout == BFLA_KV_PAGED) {
-    if (kv->page_size < 1) return fail(BFLA_ERR_INVALID_ARG, "page_size %d < 1", kv->page_size);
+    if (kv->page_size < 16 || (kv->page_size & (kv->page_size - 1)))
+      return fail(BFLA_ERR_UNSUPPORTED, "page_size %d is not a power of two >= 16",
+                  kv->page_size);
+    if (kv->n_pages < 1) return fail(BFLA_ERR_INVALID_ARG, "n_pages %lld < 1",
+                                     (long long)kv->n_pages);
+    if ((kv->n_pages - 1) * kv->page_stride + (int64_t)kv->page_size * kv->stride_tok >=
+        (int64_t(1) << 30))
+      return fail(BFLA_ERR_UNSUPPORTED, "page pool spans >= 2 GiB");
     if (!kv->block_table) return fail(BFLA_ERR_INVALID_ARG, "block_table is NULL");
     if (kv->page_stride % 8 || kv->page_stride < 1)
       return fail(BFLA_ERR_INVALID_ARG, "page_stride must be a positive multiple of 8");
@@ -177,6 +184,8 @@ KvAddr kv_addr(const bfla_kv* kv) {
     a.page_stride = kv->page_stride;
     a.page_size = kv->page_size;
     a.max_pages = kv->max_pages;
+    a.pool_bytes = (uint32_t)(((kv->n_pages - 1) * kv->page_stride +
+                               (int64_t)kv->page_size * kv->stride_tok) * 2);
   }
   return a;
 }

@@ -47,7 +47,7 @@ struct KvAddr {
   int64_t page_stride;
   int32_t page_size, max_pages;
   int32_t paged;
-  int32_t pad_;
+  uint32_t pool_bytes;  // paged: bytes from the pool base to the end of its last page
 };
 
 // Element offset of (request, kv head, token) relative to the K or V base.

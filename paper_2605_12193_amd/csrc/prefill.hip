@@ -121,12 +121,22 @@ __device__ __forceinline__ void pin_read_ahead() {
   __builtin_amdgcn_sched_group_barrier(SG_MFMA, DEPTH, 0);
 }
 
+// Group sizes whose 2m-wave workgroup would put 3 waves on a SIMD (and cap
+// registers below what the loop needs) run half q-tiles instead: m waves of
+// 32 queries, one per head, still sharing every K/V tile across the group.
+template <int M>
+struct Shape {
+  static constexpr bool HALF = (M == 5);
+  static constexpr int WAVES = HALF ? M : 2 * M;
+};
+
 template <int C, int M, bool DENSE, bool PAGED>
-__global__ void __launch_bounds__(128 * M)
+__global__ void __launch_bounds__(64 * Shape<M>::WAVES)
 prefill_kernel(PrefillArgs a) {
   using CF = Cfg<C>;
-  constexpr bool PP = CF::PING_PONG && M >= 4;  // both groups need >= 4 waves
-  constexpr int NT = 128 * M;
+  constexpr bool HALF = Shape<M>::HALF;
+  constexpr bool PP = CF::PING_PONG && !HALF && M >= 4;  // both groups need >= 4 waves
+  constexpr int NT = 64 * Shape<M>::WAVES;
   constexpr int KC_PER_T = (CF::K_CHUNKS + NT - 1) / NT;
   constexpr int VU_PER_T = (CF::V_UNITS + NT - 1) / NT;
   constexpr int NKC = C / 16;   // 16-channel chunks of the QK^T contraction
@@ -148,9 +158,10 @@ prefill_kernel(PrefillArgs a) {
   const int64_t q_off = Rd.q_off, o_off = Rd.o_off, kv_off = Rd.kv_off, lse_off = Rd.lse_off;
   const int bt_row = Rd.bt_row;
   const int local = w - Rd.work_begin;
-  const int row = Rd.row_base + (local % a.h_kv) * t_q + (t_q - 1 - local / a.h_kv);
   const int h = local % a.h_kv;
-  const int qt = t_q - 1 - local / a.h_kv;
+  const int rank = local / a.h_kv;
+  const int qt = t_q - 1 - (HALF ? rank >> 1 : rank);
+  const int row = Rd.row_base + h * t_q + qt;
   const int n_c = n_kv - n_q;
 
   int list_begin = 0, n_tiles;
@@ -162,11 +173,12 @@ prefill_kernel(PrefillArgs a) {
   }
 
   // ---- this wave's queries ----
-  const int p = h * a.m + (wave >> 1);
-  const int t = qt * TILE + (wave & 1) * 32 + l32;   // query index in request
+  const int p = h * a.m + (HALF ? wave : wave >> 1);
+  const int half = HALF ? (rank & 1) : (wave & 1);
+  const int t = qt * TILE + half * 32 + l32;          // query index in request
   const bool q_ok = t < n_q;
   const int q_pos = n_c + t;                          // absolute position
-  const int wave_q0 = n_c + qt * TILE + (wave & 1) * 32;
+  const int wave_q0 = n_c + qt * TILE + half * 32;
   const int key_lim = min(q_pos, n_kv - 1);           // last admissible key
 
   bf16x8 qf[NKC];
@@ -184,6 +196,9 @@ prefill_kernel(PrefillArgs a) {
   __builtin_amdgcn_s_waitcnt(VMCNT0);
 
   // ---- K/V addressing ----
+  // Contiguous: one descriptor per head spanning its N_kv rows.  Paged: one
+  // descriptor over the whole pool (offset by the head); keys past N_kv and
+  // table entries outside the pool land outside the range and read zeros.
   const int64_t st = a.kv.stride_tok;
   __amdgpu_buffer_rsrc_t krs, vrs;
   if (!PAGED) {
@@ -191,7 +206,15 @@ prefill_kernel(PrefillArgs a) {
     const uint32_t bytes = (uint32_t)(((int64_t)(n_kv - 1) * st + C) * 2);
     krs = make_rsrc(a.kv.k + head_off, bytes);
     vrs = make_rsrc(a.kv.v + head_off, bytes);
+  } else {
+    const int64_t head_off = (int64_t)h * a.kv.stride_head;
+    krs = make_rsrc(a.kv.k + head_off, a.kv.pool_bytes);
+    vrs = make_rsrc(a.kv.v + head_off, a.kv.pool_bytes);
   }
+  const int ps = a.kv.page_size;  // power of two >= 16
+  const int ps_shift = __builtin_ctz(ps);
+  const uint32_t page_bytes = (uint32_t)(a.kv.page_stride * 2);
+  const int32_t* bt = a.kv.block_table + (int64_t)bt_row * a.kv.max_pages;
   // per-thread constant parts of the staging pattern
   int k_row[KC_PER_T], k_ce[KC_PER_T];
   uint32_t k_boff[KC_PER_T];  // byte offset inside a contiguous tile
@@ -219,10 +242,14 @@ prefill_kernel(PrefillArgs a) {
   uint4 kreg[KC_PER_T];
   uint4 vreg[VU_PER_T][2];
 
-  auto paged_elem = [&](int key) -> int64_t {
-    int page = a.kv.block_table[(int64_t)bt_row * a.kv.max_pages + key / a.kv.page_size];
-    return (int64_t)page * a.kv.page_stride + (int64_t)(key % a.kv.page_size) * st +
-           (int64_t)h * a.kv.stride_head;
+  // Byte offset of (key, 8-channel chunk ce) in a paged pool, given the page
+  // numbers of the tile's (up to 4) pages read as scalars.
+  auto paged_off = [&](int tok0, int kr, int ce, const int* pg) -> uint32_t {
+    const int key = tok0 + kr;
+    if (key >= n_kv) return 0x80000000u;
+    const int slot = ps >= TILE ? 0 : (kr >> ps_shift);
+    const int page = slot == 0 ? pg[0] : slot == 1 ? pg[1] : slot == 2 ? pg[2] : pg[3];
+    return (uint32_t)page * page_bytes + (uint32_t)(((key & (ps - 1)) * st + 8 * ce) * 2);
   };
 
   auto load_tile = [&](int kt) {
@@ -243,24 +270,25 @@ prefill_kernel(PrefillArgs a) {
         }
       return;
     }
+    // paged: the tile's page numbers (a bad tile reads page -1 -> zeros)
+    const int tok0 = ok ? kt * TILE : 0;
+    int pg[4];
 #pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) {
-      kreg[i] = make_uint4(0, 0, 0, 0);
-      if ((CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS) && ok) {
-        const int key = kt * TILE + k_row[i];
-        if (key < n_kv) kreg[i] = ld16(a.kv.k + paged_elem(key) + 8 * k_ce[i]);
-      }
+    for (int j = 0; j < 4; ++j) {
+      const int tk = tok0 + (j << ps_shift);
+      const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
+      pg[j] = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
     }
 #pragma unroll
-    for (int i = 0; i < VU_PER_T; ++i) {
-      vreg[i][0] = make_uint4(0, 0, 0, 0);
-      vreg[i][1] = make_uint4(0, 0, 0, 0);
-      if ((CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) && ok) {
-        const int key = kt * TILE + 2 * v_j[i];
-        if (key < n_kv) vreg[i][0] = ld16(a.kv.v + paged_elem(key) + 8 * v_ce[i]);
-        if (key + 1 < n_kv) vreg[i][1] = ld16(a.kv.v + paged_elem(key + 1) + 8 * v_ce[i]);
+    for (int i = 0; i < KC_PER_T; ++i)
+      if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+        kreg[i] = bload16(krs, paged_off(tok0, k_row[i], k_ce[i], pg));
+#pragma unroll
+    for (int i = 0; i < VU_PER_T; ++i)
+      if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+        vreg[i][0] = bload16(vrs, paged_off(tok0, 2 * v_j[i], v_ce[i], pg));
+        vreg[i][1] = bload16(vrs, paged_off(tok0, 2 * v_j[i] + 1, v_ce[i], pg));
       }
-    }
   };
 
   auto store_tile = [&](bf16_t* stg) {
@@ -514,7 +542,7 @@ hipError_t launch_one(const PrefillArgs& a, int n_work, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(n_work), dim3(128 * M), lds, s, a);
+  hipLaunchKernelGGL(kern, dim3(n_work), dim3(64 * Shape<M>::WAVES), lds, s, a);
   return hipGetLastError();
 }
 
@@ -564,10 +592,12 @@ hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
   a.m = L.h_q / L.h_kv;
   a.scale = L.scale;
   a.batch = L.batch;
+  // work items per (request, KV head, q-tile): two half q-tiles for m = 5
+  const int per_row = a.m == 5 ? 2 : 1;
   int n_work = 0;
   for (int i = 0; i < a.batch.n_req; ++i) {
     a.batch.r[i].work_begin = n_work;
-    n_work += a.h_kv * a.batch.r[i].t_q;
+    n_work += per_row * a.h_kv * a.batch.r[i].t_q;
   }
   if (n_work == 0) return hipSuccess;
   const bool dense = L.row_ptr == nullptr;

@@ -94,7 +94,8 @@ def _fake_views():
     below fails validation before any launch."""
     addr = 1 << 20
     v = bfla.bfla_view(addr, None, 0, 256 * 64, 64)
-    kv = bfla.bfla_kv(bfla.BFLA_KV_CONTIGUOUS, addr, addr, None, 0, 256 * 64, 64, 0, 0, 0, None)
+    kv = bfla.bfla_kv(bfla.BFLA_KV_CONTIGUOUS, addr, addr, None, 0, 256 * 64, 64, 0, 0, 0, None,
+                      0)
     return v, kv
 
 
@@ -135,7 +136,19 @@ def test_entry_points_reject_before_launch():
     assert st == bfla.BFLA_ERR_UNSUPPORTED
     # paged K/V with too few pages in the table
     pk = bfla.bfla_kv(bfla.BFLA_KV_PAGED, 1 << 20, 1 << 20, None, 0, 64, 128, 16, 8, 16 * 128,
-                      1 << 20)
+                      1 << 20, 64)
     st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
                               None, None)
     assert st == bfla.BFLA_ERR_INVALID_ARG
+    # page size not a power of two >= 16
+    pk.max_pages = 64
+    pk.page_size = 24
+    st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
+                              None, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
+    # pool of 2 GiB or more
+    pk.page_size = 16
+    pk.n_pages = 1 << 20
+    st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
+                              None, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
