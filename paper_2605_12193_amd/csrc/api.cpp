@@ -184,6 +184,7 @@ KvAddr kv_addr(const bfla_kv* kv) {
     a.page_stride = kv->page_stride;
     a.page_size = kv->page_size;
     a.max_pages = kv->max_pages;
+    a.n_pages = (int32_t)kv->n_pages;
     a.pool_bytes = (uint32_t)(((kv->n_pages - 1) * kv->page_stride +
                                (int64_t)kv->page_size * kv->stride_tok) * 2);
   }
@@ -334,6 +335,12 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   if (!estimate_supported(prob->head_dim, params->block, params->group))
     return fail(BFLA_ERR_UNSUPPORTED, "block %d / group %d not built for head_dim %d",
                 params->block, params->group, prob->head_dim);
+  if (!estimate_q_fits(params->group, prob->head_dim, q->stride_tok))
+    return fail(BFLA_ERR_UNSUPPORTED, "q stride_tok %lld too large for group %d",
+                (long long)q->stride_tok, params->group);
+  if (kv->layout == BFLA_KV_PAGED && !estimate_pages_fit(params->group, kv->page_size))
+    return fail(BFLA_ERR_UNSUPPORTED, "group %d spans too many pages of size %d",
+                params->group, kv->page_size);
   for (int r = 0; r < prob->batch; ++r)
     if (cdiv(prob->n_kv[r], params->block) > kMaxBlocksPerRow)
       return fail(BFLA_ERR_UNSUPPORTED, "request %d: more than %d KV blocks", r,

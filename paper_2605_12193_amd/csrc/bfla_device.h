@@ -48,6 +48,8 @@ struct KvAddr {
   int32_t page_size, max_pages;
   int32_t paged;
   uint32_t pool_bytes;  // paged: bytes from the pool base to the end of its last page
+  int32_t n_pages;      // paged: valid page numbers are [0, n_pages)
+  int32_t pad_;
 };
 
 // Element offset of (request, kv head, token) relative to the K or V base.

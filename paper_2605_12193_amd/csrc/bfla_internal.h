@@ -55,6 +55,10 @@ struct EstimateLaunch {
 };
 
 bool estimate_supported(int head_dim, int block, int group);
+// Stage-1 address limits: the query rows of one score tile must span < 2 GiB,
+// and one tile's keys of a paged cache at most PT_MAX pages.
+bool estimate_q_fits(int group, int head_dim, int64_t q_stride_tok);
+bool estimate_pages_fit(int group, int page_size);
 hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream);
 
 }  // namespace bfla

@@ -28,7 +28,6 @@ namespace {
 constexpr int BM = 128;     // query groups per tile
 constexpr int BN = 128;     // key groups per tile
 constexpr int BK = 64;      // inner elements per stage
-constexpr int PITCH = BK + 8;
 constexpr int NT = 256;
 constexpr int CHAIN = 8;    // stages per inner accumulation chain (32 MFMA k-steps)
 constexpr int MAX_LKV = 65536;
@@ -63,69 +62,155 @@ __device__ __forceinline__ uint4 ld16(const bf16_t* p) {
 
 __host__ __device__ __forceinline__ int tiles_of(int groups) { return (groups + BM - 1) / BM; }
 
-template <int G>
-__global__ void __launch_bounds__(NT, 2) scores_kernel(ScoreArgs a) {
-  __shared__ __align__(16) bf16_t sa[2][BM * PITCH];
-  __shared__ __align__(16) bf16_t sb[2][BN * PITCH];
+// One operand tile of one ring stage: 128 rows x 64 bf16 (128 B per row, no
+// padding).  Rows are XOR-swizzled in 16-byte chunks (physical chunk =
+// logical chunk ^ ((row / 2) % 8)) so that the 32x32 fragment reads of 16
+// consecutive rows hit 16 distinct bank groups.
+constexpr int STAGE_ELEMS = BM * BK;
+constexpr int NSTAGE = 4;     // ring depth: loads run NSTAGE - 1 stages ahead
+constexpr uint32_t RSRC_WORD3 = 0x00020000u;
+constexpr int PT_MAX = 2048;  // page-table entries one tile of a paged cache may span
+constexpr uint32_t BAD_PAGE = 0xFFFFFFFFu;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor (stride 0, byte range [0, bytes)): offsets at or past
+// `bytes` read as zeros.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(b >> 32) & 0xFFFF);
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = (int)RSRC_WORD3;
+  return r;
+}
+
+// 16 bytes per lane from a buffer straight into LDS: lane l writes
+// [lds + 16 l, +16).  Issued as inline assembly so that the compiler adds no
+// waits of its own; the caller waits (vmcnt) and synchronises before the
+// data are read.
+__device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(rs)
+               : "memory", "m0");
+}
+
+#define LDS_ADDR(arr) ((uint32_t)(uintptr_t)(lds_ptr_t)(arr))
+
+template <int G, bool PAGED>
+__global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
+  // ring slot s: Q tile at ring[s][0], K tile at ring[s][1]
+  __shared__ __align__(1024) bf16_t ring[NSTAGE][2][STAGE_ELEMS];
+  __shared__ uint32_t page_base[PAGED ? PT_MAX : 1];  // byte offset of each page, or BAD_PAGE
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hi = lane >> 5;
   const int wi = wave >> 1, wj = wave & 1;
 
   // ---- tile decode: (request, tile rank, head) with the KV head fastest ----
   const int ri = find_req(a.batch, blockIdx.x);
   const ReqDesc& R = a.batch.r[ri];
+  const int n_q = R.n_q, n_kv = R.n_kv;
+  const int64_t q_off = R.q_off, kv_off = R.kv_off;
+  const int bt_row = R.bt_row;
   const int local = blockIdx.x - R.work_begin;
-  const int nqg = (R.n_q + a.g - 1) / a.g;    // query groups
-  const int nkg = (R.n_kv + a.g - 1) / a.g;   // key groups
+  const int nqg = (n_q + a.g - 1) / a.g;    // query groups
+  const int nkg = (n_kv + a.g - 1) / a.g;   // key groups
   const int ntj = tiles_of(nkg);
   const int h = local % a.h_kv;
   const int pm = (local / a.h_kv) % a.m;
   const int rank = local / a.h_q;
   const int ti = rank / ntj, tj = rank % ntj;
   const int p = h * a.m + pm;
-  const int n_c = R.n_kv - R.n_q;
+  const int n_c = n_kv - n_q;
 
   // skip tiles without any causal block pair
   {
     int gi_last = min(nqg, (ti + 1) * BM) - 1;
     int i_max = gi_last / G;
-    int e_i = min(n_c + (i_max + 1) * a.b - 1, R.n_kv - 1);
+    int e_i = min(n_c + (i_max + 1) * a.b - 1, n_kv - 1);
     int j_min = (tj * BN) / G;
     if (j_min * a.b > e_i) return;
   }
 
-  const bf16_t* qbase = a.q + R.q_off + (int64_t)p * a.q_sh;
-  const int n_stage = a.gc / BK;
-
-  // loader mapping: 1024 16-byte chunks per operand tile, 4 per thread
-  uint4 ra[4], rbv[4];
-  auto load = [&](int st) {
+  // ---- direct global -> LDS loads through buffer descriptors ----
+  // Wave w, load i (0..3) fills rows [8 (4 i + w), +8) of a stage: lane l
+  // writes LDS chunk l % 8 of row 8 (4 i + w) + l / 8 and fetches the
+  // logical chunk that the swizzle places there.  Out-of-range offsets
+  // (padding groups, tokens past the end, bad pages) read as zeros.  The Q
+  // descriptor starts at the tile's first query token, so it spans at most
+  // BM * g token rows.
+  const int q_tok0 = ti * BM * a.g;
+  const int q_tile_tok = min(n_q - q_tok0, BM * a.g);
+  const i32x4 qrs =
+      make_rsrc(a.q + q_off + (int64_t)p * a.q_sh + (int64_t)q_tok0 * a.q_st,
+                (uint32_t)(((int64_t)(q_tile_tok - 1) * a.q_st + a.C) * 2));
+  const i32x4 krs =
+      make_rsrc(a.kv.k + (PAGED ? 0 : kv_off) + (int64_t)h * a.kv.stride_head,
+                PAGED ? a.kv.pool_bytes
+                      : (uint32_t)(((int64_t)(n_kv - 1) * a.kv.stride_tok + a.C) * 2));
+  const int ps_shift = PAGED ? __builtin_ctz(a.kv.page_size) : 0;
+  const int k_tok0 = tj * BN * a.g;                 // first key token of the tile (< n_kv)
+  const int first_page = k_tok0 >> ps_shift;
+  if (PAGED) {
+    // the pages this tile's keys live in, resolved once: byte offset of each
+    // page in the pool, or BAD_PAGE for an entry outside [0, n_pages)
+    const int32_t* bt = a.kv.block_table + (int64_t)bt_row * a.kv.max_pages;
+    const int n_pt = ((min(n_kv, k_tok0 + BN * a.g) - 1) >> ps_shift) - first_page + 1;
+    const uint32_t page_bytes = (uint32_t)(a.kv.page_stride * 2);
+    for (int e = tid; e < n_pt; e += NT) {
+      const int pg = bt[first_page + e];
+      page_base[e] = (unsigned)pg < (unsigned)a.kv.n_pages ? (uint32_t)pg * page_bytes : BAD_PAGE;
+    }
+    __syncthreads();
+  }
+  const int row_sub = lane >> 3, pch = lane & 7;
+  int q_row_tok[4], k_row_tok[4];   // first token of the group of each loaded row
+  int lch[4];                       // logical chunk fetched by this lane
+  bool q_ok[4], k_ok[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 8 * (4 * i + wave) + row_sub;
+    lch[i] = swz(row, pch);
+    const int gi = ti * BM + row, gj = tj * BN + row;
+    q_ok[i] = gi < nqg;
+    k_ok[i] = gj < nkg;
+    q_row_tok[i] = row * a.g;   // relative to q_tok0
+    k_row_tok[i] = gj * a.g;
+  }
+  const uint32_t ring_lds = LDS_ADDR(&ring[0][0][0]) + (uint32_t)wave * 1024;
+  constexpr uint32_t SLOT_BYTES = 2 * STAGE_ELEMS * 2;
+  auto issue = [&](int st) __attribute__((always_inline)) {
+    const uint32_t la = ring_lds + (uint32_t)(st % NSTAGE) * SLOT_BYTES;
+    const uint32_t lb = la + STAGE_ELEMS * 2;
     const int k0 = st * BK;
     const int tok_in = k0 / a.C, ch = k0 % a.C;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int e = tid + i * NT;
-      const int row = e >> 3, ce = e & 7;
-      const int gi = ti * BM + row;
-      const int tq = gi * a.g + tok_in;
-      ra[i] = (gi < nqg && tq < R.n_q)
-                  ? ld16(qbase + (int64_t)tq * a.q_st + ch + 8 * ce)
-                  : make_uint4(0, 0, 0, 0);
-      const int gj = tj * BN + row;
-      const int tk = gj * a.g + tok_in;
-      rbv[i] = (gj < nkg && tk < R.n_kv)
-                   ? ld16(a.kv.k + kv_elem(a.kv, R, h, tk) + ch + 8 * ce)
-                   : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = tid + i * NT;
-      const int row = e >> 3, ce = e & 7;
-      *reinterpret_cast<uint4*>(&sa[buf][row * PITCH + 8 * ce]) = ra[i];
-      *reinterpret_cast<uint4*>(&sb[buf][row * PITCH + 8 * ce]) = rbv[i];
+      const int tq = q_row_tok[i] + tok_in;
+      const uint32_t qo = (q_ok[i] && tq < q_tile_tok)
+                              ? (uint32_t)(((int64_t)tq * a.q_st + ch + 8 * lch[i]) * 2)
+                              : 0x80000000u;
+      dma16(qrs, la + i * 4096, qo);
+      const int tk = k_row_tok[i] + tok_in;
+      uint32_t ko = 0x80000000u;
+      if (k_ok[i] && tk < n_kv) {
+        if (PAGED) {
+          const uint32_t pb = page_base[(tk >> ps_shift) - first_page];
+          if (pb != BAD_PAGE)
+            ko = pb + (uint32_t)((((tk & (a.kv.page_size - 1)) * a.kv.stride_tok) + ch +
+                                  8 * lch[i]) * 2);
+        } else {
+          ko = (uint32_t)(((int64_t)tk * a.kv.stride_tok + ch + 8 * lch[i]) * 2);
+        }
+      }
+      dma16(krs, lb + i * 4096, ko);
     }
   };
 
@@ -137,38 +222,57 @@ __global__ void __launch_bounds__(NT, 2) scores_kernel(ScoreArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) { acc[x][y][r] = 0.f; tot[x][y][r] = 0.f; }
 
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int st = 0; st < n_stage; ++st) {
-    const bool more = st + 1 < n_stage;
-    if (more) load(st + 1);
-    const bf16_t* A = sa[st & 1];
-    const bf16_t* B = sb[st & 1];
+  const int n_stage = a.gc / BK;
+  auto compute = [&](const bf16_t* A, const bf16_t* B) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 af[2], bf[2];
 #pragma unroll
-      for (int x = 0; x < 2; ++x)
-        af[x] = __builtin_bit_cast(bf16x8, ld16(A + (64 * wi + 32 * x + l32) * PITCH + 16 * ks + 8 * hi));
+      for (int x = 0; x < 2; ++x) {
+        const int row = 64 * wi + 32 * x + l32;
+        af[x] = __builtin_bit_cast(bf16x8, ld16(A + row * BK + 8 * swz(row, 2 * ks + hi)));
+      }
 #pragma unroll
-      for (int y = 0; y < 2; ++y)
-        bf[y] = __builtin_bit_cast(bf16x8, ld16(B + (64 * wj + 32 * y + l32) * PITCH + 16 * ks + 8 * hi));
+      for (int y = 0; y < 2; ++y) {
+        const int row = 64 * wj + 32 * y + l32;
+        bf[y] = __builtin_bit_cast(bf16x8, ld16(B + row * BK + 8 * swz(row, 2 * ks + hi)));
+      }
 #pragma unroll
       for (int x = 0; x < 2; ++x)
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(af[x], bf[y], acc[x][y]);
     }
-    if ((st + 1) % CHAIN == 0 || !more) {
-#pragma unroll
-      for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) { tot[x][y][r] += acc[x][y][r]; acc[x][y][r] = 0.f; }
+  };
+  // s_waitcnt immediates: vmcnt(n) with the other counters left free
+  constexpr int VM16 = 0x4F70, VM8 = 0x0F78, VM0 = 0x0F70;
+
+  // prologue: stages 0 .. NSTAGE - 2 in flight
+  for (int st = 0; st < NSTAGE - 1 && st < n_stage; ++st) issue(st);
+  for (int c0 = 0; c0 < n_stage; c0 += CHAIN) {
+    const int c1 = min(c0 + CHAIN, n_stage);
+    for (int st = c0; st < c1; ++st) {
+      // this wave's loads of stage st are done once at most the loads of the
+      // stages after it (up to NSTAGE - 2, 8 each) remain; the barrier then
+      // makes every wave's part visible, and also tells that every wave is
+      // done reading the slot refilled next (stage st - 1's)
+      const int ahead = min(NSTAGE - 2, n_stage - 1 - st);
+      if (ahead == 2) __builtin_amdgcn_s_waitcnt(VM16);
+      else if (ahead == 1) __builtin_amdgcn_s_waitcnt(VM8);
+      else __builtin_amdgcn_s_waitcnt(VM0);
+      // plain barrier: a __syncthreads() fence would also wait for the
+      // loads still in flight for the later stages
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      if (st + NSTAGE - 1 < n_stage) issue(st + NSTAGE - 1);
+      const int slot = st % NSTAGE;
+      compute(&ring[slot][0][0], &ring[slot][1][0]);
     }
-    if (more) store((st + 1) & 1);
-    __syncthreads();
+    // close the chain: fold it into the running total
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) { tot[x][y][r] += acc[x][y][r]; acc[x][y][r] = 0.f; }
   }
 
   // ---- epilogue: drop padded groups, G x G max pool, causal store ----
@@ -293,7 +397,10 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
 
 template <int G>
 hipError_t launch_scores(const ScoreArgs& a, int n_tiles, hipStream_t s) {
-  hipLaunchKernelGGL(scores_kernel<G>, dim3(n_tiles), dim3(NT), 0, s, a);
+  if (a.kv.paged)
+    hipLaunchKernelGGL((scores_kernel<G, true>), dim3(n_tiles), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL((scores_kernel<G, false>), dim3(n_tiles), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -305,6 +412,15 @@ bool estimate_supported(int head_dim, int block, int group) {
   const int G = block / group;
   if (G != 1 && G != 2 && G != 4 && G != 8) return false;
   return ((int64_t)group * head_dim) % BK == 0;
+}
+
+bool estimate_q_fits(int group, int head_dim, int64_t q_stride_tok) {
+  return ((int64_t)BM * group - 1) * q_stride_tok + head_dim < (int64_t(1) << 30);
+}
+
+bool estimate_pages_fit(int group, int page_size) {
+  // a tile of BN key groups covers BN * g tokens: at most BN * g / ps + 1 pages
+  return ((int64_t)BN * group + page_size - 1) / page_size + 1 <= PT_MAX;
 }
 
 hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {

@@ -278,6 +278,7 @@ prefill_kernel(PrefillArgs a) {
       const int tk = tok0 + (j << ps_shift);
       const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
       pg[j] = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
+      if ((unsigned)pg[j] >= (unsigned)a.kv.n_pages) pg[j] = -1;  // entry outside the pool
     }
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
