@@ -173,8 +173,10 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
  *   block_mask  out, device uint8, layout above.
  *   dbg_scores  out, device float or NULL.
  *   workspace   device scratch of >= bfla_workspace_size(BFLA_WS_ESTIMATE).
- * Errors: INVALID_ARG, UNSUPPORTED (also more than 65536 KV blocks per
- * request), WORKSPACE, HIP. */
+ * Errors: INVALID_ARG, UNSUPPORTED (also: more than 65536 KV blocks per
+ * request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
+ * i.e. (128 g - 1) * stride_tok + head_dim >= 2^30; paged K where 128 g
+ * tokens may span more than 2048 pages), WORKSPACE, HIP. */
 int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params,
                        const bfla_view* q, const bfla_kv* kv,
                        uint8_t* block_mask, float* dbg_scores,

@@ -7,7 +7,8 @@
 // are flattened key groups (inner dimension g*C; a flattened group of a
 // row-major [N][C] head is g consecutive token rows, so no copy is made,
 // eq6-eq7).  128 x 128 output tiles, 4 waves of 64 x 64, bf16 MFMA
-// 32x32x16, K/Q chunks staged through LDS with register double buffering;
+// 32x32x16; Q/K chunks of 64 inner elements go from buffer loads straight
+// into a 4-slot LDS ring (three chunks in flight, one workgroup per CU);
 // only tiles holding a causal block pair are computed (eq11-eq14).  The
 // epilogue max-pools each G x G group block into the block score (eq10)
 // and stores it as float.  Accumulation is two-level: chains of 32 MFMA

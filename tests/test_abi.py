@@ -152,3 +152,24 @@ def test_entry_points_reject_before_launch():
     st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
                               None, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
+
+
+def test_estimate_address_limits():
+    L = bfla.lib()
+    addr = C.c_void_p(1 << 20)
+    p, prm = _prob(), bfla.params()
+    _, kv = _fake_views()
+    # q rows of one score tile (128 groups of 64 tokens) spanning >= 2 GiB
+    wide = bfla.bfla_view(1 << 20, None, 0, 64, 1 << 18)
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(wide), C.byref(kv), addr,
+                              addr, None, 0, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
+    # paged K: 128 groups of 512 tokens cover 4097 16-token pages
+    big = bfla.params(block=1024, group=512)
+    pk = bfla.bfla_kv(bfla.BFLA_KV_PAGED, 1 << 20, 1 << 20, None, 0, 64, 128, 16, 64, 16 * 128,
+                      1 << 20, 64)
+    q = bfla.bfla_view(1 << 20, None, 0, 256 * 64, 64)
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(big), C.byref(q), C.byref(pk), addr, addr,
+                              None, 0, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
+    assert "pages" in L.bfla_last_error().decode()
