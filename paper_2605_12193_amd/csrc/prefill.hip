@@ -121,22 +121,25 @@ __device__ __forceinline__ void pin_read_ahead() {
   __builtin_amdgcn_sched_group_barrier(SG_MFMA, DEPTH, 0);
 }
 
-// Group sizes whose 2m-wave workgroup would put 3 waves on a SIMD (and cap
-// registers below what the loop needs) run half q-tiles instead: m waves of
-// 32 queries, one per head, still sharing every K/V tile across the group.
-template <int M>
+// Shapes whose 2m-wave workgroup would cap registers below what the loop
+// needs run half q-tiles instead: m waves of 32 queries, one per head, still
+// sharing every K/V tile across the group.  That is m = 5 (3 waves on a SIMD)
+// and m = 8 (16 waves), and m = 4 at C = 256 (two waves per SIMD cannot hold
+// the 256-channel accumulators).
+template <int C, int M>
 struct Shape {
-  static constexpr bool HALF = (M == 5);
+  static constexpr bool HALF = (M == 5 || M == 8 || (C == 256 && M == 4));
   static constexpr int WAVES = HALF ? M : 2 * M;
 };
 
 template <int C, int M, bool DENSE, bool PAGED>
-__global__ void __launch_bounds__(64 * Shape<M>::WAVES)
+__global__ void __launch_bounds__(64 * (Shape<C, M>::WAVES))
 prefill_kernel(PrefillArgs a) {
   using CF = Cfg<C>;
-  constexpr bool HALF = Shape<M>::HALF;
-  constexpr bool PP = CF::PING_PONG && !HALF && M >= 4;  // both groups need >= 4 waves
-  constexpr int NT = 64 * Shape<M>::WAVES;
+  constexpr bool HALF = Shape<C, M>::HALF;
+  // ping-pong needs two groups of 4 waves, one wave of each per SIMD
+  constexpr bool PP = CF::PING_PONG && Shape<C, M>::WAVES == 8;
+  constexpr int NT = 64 * Shape<C, M>::WAVES;
   constexpr int KC_PER_T = (CF::K_CHUNKS + NT - 1) / NT;
   constexpr int VU_PER_T = (CF::V_UNITS + NT - 1) / NT;
   constexpr int NKC = C / 16;   // 16-channel chunks of the QK^T contraction
@@ -543,7 +546,7 @@ hipError_t launch_one(const PrefillArgs& a, int n_work, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3(n_work), dim3(64 * Shape<M>::WAVES), lds, s, a);
+  hipLaunchKernelGGL(kern, dim3(n_work), dim3(64 * Shape<C, M>::WAVES), lds, s, a);
   return hipGetLastError();
 }
 
@@ -593,8 +596,9 @@ hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
   a.m = L.h_q / L.h_kv;
   a.scale = L.scale;
   a.batch = L.batch;
-  // work items per (request, KV head, q-tile): two half q-tiles for m = 5
-  const int per_row = a.m == 5 ? 2 : 1;
+  // work items per (request, KV head, q-tile): two for the half-tile shapes
+  const bool half = a.m == 5 || a.m == 8 || (L.head_dim == 256 && a.m == 4);
+  const int per_row = half ? 2 : 1;
   int n_work = 0;
   for (int i = 0; i < a.batch.n_req; ++i) {
     a.batch.r[i].work_begin = n_work;

@@ -27,6 +27,9 @@ SHAPES = [
     ("mha_m1", [512 + 64 + 5], None, 2, 2, 128),
     ("gqa8", [640], None, 8, 1, 64),
     ("batch3", [900, 300, 1200], [900, 100, 1200], 4, 2, 64),
+    ("gqa4_c64_chunked", [1300], [700], 8, 2, 64),
+    ("gqa8_c128", [900], None, 8, 1, 128),
+    ("wide_gqa4", [700], [500], 8, 2, 256),
 ]
 IDS = [s[0] for s in SHAPES]
 
