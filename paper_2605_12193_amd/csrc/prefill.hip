@@ -21,6 +21,8 @@
 // read through buffer descriptors whose range check returns zeros past the
 // last key, so loads carry no branches.
 //
+// The lane ^ 32 exchanges of the row max and sum use v_permlane32_swap.
+//
 // The online softmax keeps a stale running max: O and l are rescaled only
 // when a row's max grows by more than 2^RESCALE_LOG2 in the exp2 domain.
 // Both are always scaled by the same max, so O / l is exact, and every
@@ -81,6 +83,23 @@ __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   f32x2 x = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+}
+
+// max / sum of x over lanes l and l ^ 32, in every lane, without going
+// through LDS: v_permlane32_swap leaves x of lane l % 32 in one result and
+// x of lane 32 + l % 32 in the other.
+__device__ __forceinline__ f32x2 lane32_pair(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
+                                                  __builtin_bit_cast(uint32_t, x), false, false);
+  return f32x2{__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1])};
+}
+__device__ __forceinline__ float max_lane32(float x) {
+  const f32x2 p = lane32_pair(x);
+  return fmaxf(p[0], p[1]);
+}
+__device__ __forceinline__ float add_lane32(float x) {
+  const f32x2 p = lane32_pair(x);
+  return p[0] + p[1];
 }
 
 // Position of key offset k (0..63) inside the permuted V^T row.
@@ -377,7 +396,7 @@ prefill_kernel(PrefillArgs a) {
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = max_lane32(mx);
     // move the stale max only when the new max exceeds it by 2^RESCALE_LOG2
     const bool grow = (mx - m_run) * c2 > RESCALE_LOG2 || (m_run == -INFINITY && mx != -INFINITY);
     if (__builtin_amdgcn_ballot_w64(grow)) {
@@ -399,8 +418,7 @@ prefill_kernel(PrefillArgs a) {
       rs0 += s0[r];
       rs1 += s1[r];
     }
-    float rs = rs0 + rs1;
-    rs += __shfl_xor(rs, 32);
+    const float rs = add_lane32(rs0 + rs1);
     l_run += rs;
     // P^T (bf16) as B operands: 16-key chunk q = regs 8(q%2).. of block q/2
 #pragma unroll
