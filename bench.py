@@ -46,6 +46,10 @@ def parse():
     ap.add_argument("--workload", default="llama_128k")
     ap.add_argument("--gamma", type=float, default=None)
     ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--block", type=int, default=None, help="coarse block b")
+    ap.add_argument("--group", type=int, default=None, help="flattening group g")
+    ap.add_argument("--n-local", type=int, default=None)
+    ap.add_argument("--eta", type=int, default=None)
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="time budget of the oracle sample")
@@ -207,6 +211,10 @@ def main():
         over["gamma"] = args.gamma
     if args.rho is not None:
         over["rho"] = args.rho
+    for key, val in (("block", args.block), ("group", args.group), ("n_local", args.n_local),
+                     ("eta", args.eta)):
+        if val is not None:
+            over[key] = val
     wl = synth.workload(args.workload, **over)
     t_gen = time.perf_counter()
     torch.cuda.set_device(0)

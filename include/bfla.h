@@ -118,7 +118,7 @@ typedef struct bfla_kv {
 /* Method hyper-parameters. */
 typedef struct bfla_params {
   int32_t block;    /* b, coarse block size (eq4); multiple of tile and group */
-  int32_t group;    /* g, flattening group (eq6); b / g <= 8 */
+  int32_t group;    /* g, flattening group (eq6); b / g in {1, 2, 4, 8, 16} */
   int32_t tile;     /* T, attention tile (eq19); 64 */
   float gamma;      /* keep-mass threshold (eq17), 0 < gamma <= 1 */
   int32_t n_local;  /* local band (eq21): diagonal tile + n_local before it;

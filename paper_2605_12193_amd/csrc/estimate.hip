@@ -306,18 +306,23 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; r += 4) pr[r] = fmaxf(pr[r], __shfl_xor(pr[r], 32));
       }
+      if (G >= 16) {   // rows 8 (r / 4) .. +7 -> 16 consecutive rows
+#pragma unroll
+        for (int r = 0; r < 16; r += 8) pr[r] = fmaxf(pr[r], pr[r + 4]);
+      }
       // pool over G consecutive key-group columns (lanes)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         if (G >= 2) pr[r] = fmaxf(pr[r], __shfl_xor(pr[r], 1));
         if (G >= 4) pr[r] = fmaxf(pr[r], __shfl_xor(pr[r], 2));
         if (G >= 8) pr[r] = fmaxf(pr[r], __shfl_xor(pr[r], 4));
+        if (G >= 16) pr[r] = fmaxf(pr[r], __shfl_xor(pr[r], 8));
       }
       if ((l32 % G) != 0 || (G >= 8 && hi != 0)) continue;
       const int j = gj / G;
       if (j >= R.l_kv) continue;
 #pragma unroll
-      for (int r = 0; r < 16; r += (G >= 4 ? 4 : G)) {
+      for (int r = 0; r < 16; r += (G >= 16 ? 8 : G >= 4 ? 4 : G)) {
         const int gi = ti * BM + 64 * wi + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
         const int i = gi / G;
         if (i >= R.l_q) continue;
@@ -411,7 +416,7 @@ bool estimate_supported(int head_dim, int block, int group) {
   if (head_dim != 64 && head_dim != 128 && head_dim != 256) return false;
   if (group < 1 || block % group) return false;
   const int G = block / group;
-  if (G != 1 && G != 2 && G != 4 && G != 8) return false;
+  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16) return false;
   return ((int64_t)group * head_dim) % BK == 0;
 }
 
@@ -456,6 +461,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
     case 2: e = launch_scores<2>(a, n_tiles, stream); break;
     case 4: e = launch_scores<4>(a, n_tiles, stream); break;
     case 8: e = launch_scores<8>(a, n_tiles, stream); break;
+    case 16: e = launch_scores<16>(a, n_tiles, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

@@ -1,0 +1,71 @@
+"""Every BFLA configuration of the paper's mask-density table (Sec. 5, the
+LongBench table over b, g, gamma, n_local, rho, eta) on a Llama-shaped
+request: Stage 1 against the oracle on sure cells, the tile lists bit-exact
+against the oracle's tile stage applied to the GPU mask, and the outputs
+against the oracle's retained-tile attention."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bfla_oracle as O
+from paper_2605_12193_amd import bfla, synth
+from parity_util import DeviceBatch, compare_outputs, mask_compare, oracle_lists_for
+
+pytestmark = pytest.mark.gpu
+
+# (b, g, gamma, n_local, rho, eta); "no eta" is eta = 0
+PAPER_CONFIGS = [
+    (256, 64, 0.95, 8, 0.0, 0),
+    (256, 64, 0.999, 8, 0.0, 0),
+    (256, 64, 0.95, 8, 0.0, 16),
+    (256, 64, 0.95, 16, 0.0, 16),
+    (256, 64, 0.98, 8, 0.0, 16),
+    (256, 64, 0.99, 8, 0.0, 16),
+    (128, 64, 0.99, 8, 0.1, 16),
+    (256, 64, 0.99, 8, 0.1, 16),
+    (256, 256, 0.99, 8, 0.1, 16),
+    (512, 64, 0.99, 8, 0.1, 16),
+    (512, 128, 0.99, 8, 0.1, 16),
+    (1024, 64, 0.99, 8, 0.1, 16),
+]
+IDS = [f"b{b}_g{g}_gam{gam}_nl{nl}_rho{r}_eta{e}" for b, g, gam, nl, r, e in PAPER_CONFIGS]
+
+
+@pytest.mark.parametrize("cfg", PAPER_CONFIGS, ids=IDS)
+def test_paper_config_end_to_end(cfg):
+    b, g, gamma, n_local, rho, eta = cfg
+    n = 4500
+    wl = synth.workload("llama_32k", seqlens=[n], h_q=8, h_kv=2)
+    seqs = synth.make_inputs(wl)
+    db = DeviceBatch(seqs, None)
+    kw = dict(block=b, group=g, tile=64, gamma=gamma, n_local=n_local, n_sink=1, eta=eta,
+              rho=rho, seed=wl.seed)
+    prm = bfla.params(**kw)
+    buf = bfla.Buffers(db.prob, prm)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
+    torch.cuda.synchronize()
+    rp_gpu = buf.row_ptr.cpu().numpy()
+    assert rp_gpu[0] == 0 and np.all(np.diff(rp_gpu) >= 0) and rp_gpu[-1] <= buf.cols.numel()
+    bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, buf.row_ptr, buf.cols, db.ov, buf.lse)
+    torch.cuda.synchronize()
+
+    q, k, v = db.host(0)
+    alpha = O.default_scale(db.c)
+    st = O.estimate_mask(q, k, b, g, gamma, alpha)
+    gm = buf.block_mask.cpu().numpy()[:st["mask"].size].reshape(st["mask"].shape)
+    fin = np.isfinite(st["scores"])
+    gs = buf.scores.cpu().numpy()[:st["scores"].size].reshape(st["scores"].shape)
+    assert np.array_equal(np.isinf(gs), np.isinf(st["scores"]))
+    assert (np.abs(gs[fin].astype(np.float64) - st["scores"][fin]) * alpha).max() < 1e-4
+    ties = mask_compare(gm, st["mask"], st["status"])
+    rp, cols, _ = oracle_lists_for(db, [gm], kw)
+    assert np.array_equal(rp_gpu, rp)
+    assert np.array_equal(buf.cols.cpu().numpy()[:rp[-1]], cols)
+    want, want_lse = O.attention(q, k, v, 64, alpha, rp, cols, 0)
+    compare_outputs(db.o_of(0), want, str(cfg))
+    np.testing.assert_allclose(buf.lse.cpu().numpy().reshape(want_lse.shape), want_lse,
+                               rtol=0, atol=2e-4)
+    causal = sum(min((n - 1) // 64, qt) + 1 for qt in range(-(-n // 64))) * db.h_kv
+    print(f"{cfg}: kept {rp[-1]} of {causal} causal tiles ({rp[-1] / causal:.1%}), "
+          f"near-tie mismatches {ties}")
