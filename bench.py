@@ -200,7 +200,7 @@ def cpu_baseline(wl, inp, gpu_o, budget_s, seed=0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this library runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
 
     import torch
