@@ -52,17 +52,6 @@ struct KvAddr {
   int32_t pad_;
 };
 
-// Element offset of (request, kv head, token) relative to the K or V base.
-__device__ __forceinline__ int64_t kv_elem(const KvAddr& a, const ReqDesc& R,
-                                           int h, int t) {
-  if (a.paged) {
-    int page = a.block_table[(int64_t)R.bt_row * a.max_pages + t / a.page_size];
-    return (int64_t)page * a.page_stride + (int64_t)(t % a.page_size) * a.stride_tok +
-           (int64_t)h * a.stride_head;
-  }
-  return R.kv_off + (int64_t)h * a.stride_head + (int64_t)t * a.stride_tok;
-}
-
 // Request owning work item `w` (requests are laid out by work_begin).
 __device__ __forceinline__ int find_req(const Batch& b, int w) {
   int r = 0;
