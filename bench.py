@@ -22,6 +22,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -61,10 +62,16 @@ def parse():
 
 
 def prefill_source_hash() -> str:
+    """Hash of the prefill kernel's code (prefill.hip and the device header)
+    with comments and whitespace removed, so only code changes invalidate a
+    committed traffic profile."""
     m = hashlib.sha256()
     for f in ("paper_2605_12193_amd/csrc/prefill.hip", "paper_2605_12193_amd/csrc/bfla_device.h"):
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            m.update(fh.read())
+        with open(os.path.join(ROOT, f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        m.update(" ".join(text.split()).encode())
     return m.hexdigest()[:16]
 
 
