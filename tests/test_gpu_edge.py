@@ -1,0 +1,78 @@
+"""Degenerate and boundary inputs through the whole path against the oracle:
+sequences of 1, 2 and around one tile / one block, a single query against a
+long prefix, and the maximum batch of 32 requests of mixed lengths."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bfla_oracle as O
+from paper_2605_12193_amd import bfla, synth
+from parity_util import DeviceBatch, compare_outputs, mask_compare, oracle_lists_for
+
+pytestmark = pytest.mark.gpu
+
+KW = dict(block=128, group=64, tile=64, gamma=0.9, n_local=2, n_sink=1, eta=16, rho=0.1,
+          seed=11)
+
+
+def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
+    wl = synth.workload("tiny_2k", h_q=h_q, h_kv=h_kv, head_dim=c, seed=seed)
+    seqs = synth.make_inputs(wl, seqlens=seqlens)
+    db = DeviceBatch(seqs, n_q)
+    prm = bfla.params(**KW)
+    buf = bfla.Buffers(db.prob, prm)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
+    torch.cuda.synchronize()
+    rp_gpu = buf.row_ptr.cpu().numpy()
+    assert rp_gpu[0] == 0 and np.all(np.diff(rp_gpu) >= 0) and rp_gpu[-1] <= buf.cols.numel()
+    bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, buf.row_ptr, buf.cols, db.ov, buf.lse)
+    torch.cuda.synchronize()
+    alpha = O.default_scale(c)
+    gm_all = buf.block_mask.cpu().numpy()
+    masks, off = [], 0
+    for r in range(len(seqs)):
+        q, k, _ = db.host(r)
+        st = O.estimate_mask(q, k, KW["block"], KW["group"], KW["gamma"], alpha)
+        gm = gm_all[off:off + st["mask"].size].reshape(st["mask"].shape)
+        off += st["mask"].size
+        mask_compare(gm, st["mask"], st["status"])
+        masks.append(gm)
+    rp, cols, _ = oracle_lists_for(db, masks, KW)
+    assert np.array_equal(rp_gpu, rp)
+    assert np.array_equal(buf.cols.cpu().numpy()[:rp[-1]], cols)
+    lse = buf.lse.cpu().numpy()
+    lse_off = 0
+    for r in range(len(seqs)):
+        q, k, v = db.host(r)
+        base = sum(db.h_kv * -(-n // 64) for n in db.n_q[:r])
+        want, want_lse = O.attention(q, k, v, 64, alpha, rp, cols, base)
+        compare_outputs(db.o_of(r), want, f"request {r} of {len(seqs)}")
+        got = lse[lse_off:lse_off + h_q * db.n_q[r]].reshape(h_q, db.n_q[r])
+        lse_off += h_q * db.n_q[r]
+        np.testing.assert_allclose(got, want_lse, rtol=0, atol=2e-4)
+    # the dense kernel on the same batch
+    db.o.fill_(float("nan"))
+    bfla.bfla_dense_prefill(db.prob, prm, db.qv, db.kv, db.ov)
+    torch.cuda.synchronize()
+    for r in range(len(seqs)):
+        q, k, v = db.host(r)
+        want, _ = O.attention(q, k, v, 64, alpha)
+        compare_outputs(db.o_of(r), want, f"dense request {r} of {len(seqs)}")
+
+
+@pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 127, 128, 129])
+def test_short_sequences(n):
+    _run([n])
+
+
+@pytest.mark.parametrize("c", [64, 128])
+def test_single_query_after_long_prefix(c):
+    _run([1000], n_q=[1], h_q=8, h_kv=2, c=c)
+
+
+def test_max_batch_of_32_requests():
+    rng = np.random.default_rng(3)
+    seqlens = [int(x) for x in rng.integers(1, 700, size=32)]
+    n_q = [max(1, int(n * f)) for n, f in zip(seqlens, rng.uniform(0.3, 1.0, size=32))]
+    _run(seqlens, n_q=n_q)
