@@ -6,9 +6,9 @@
 // is a GEMM whose rows are flattened g-token query groups and whose columns
 // are flattened key groups (inner dimension g*C; a flattened group of a
 // row-major [N][C] head is g consecutive token rows, so no copy is made,
-// eq6-eq7).  128 x 128 output tiles, 4 waves of 64 x 64, bf16 MFMA
+// eq6-eq7).  256 x 128 output tiles, 4 waves of 64 x 128, bf16 MFMA
 // 32x32x16; Q/K chunks of 64 inner elements go from buffer loads straight
-// into a 4-slot LDS ring (three chunks in flight, one workgroup per CU);
+// into a 3-slot LDS ring (two chunks in flight, one workgroup per CU);
 // only tiles holding a causal block pair are computed (eq11-eq14).  The
 // epilogue max-pools each G x G group block into the block score (eq10)
 // and stores it as float.  Accumulation is two-level: chains of 32 MFMA
@@ -26,7 +26,7 @@
 namespace bfla {
 namespace {
 
-constexpr int BM = 128;     // query groups per tile
+constexpr int BM = 256;     // query groups per tile (64 per wave)
 constexpr int BN = 128;     // key groups per tile
 constexpr int BK = 64;      // inner elements per stage
 constexpr int NT = 256;
@@ -61,14 +61,19 @@ __device__ __forceinline__ uint4 ld16(const bf16_t* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
-__host__ __device__ __forceinline__ int tiles_of(int groups) { return (groups + BM - 1) / BM; }
+__host__ __device__ __forceinline__ int row_tiles(int groups) { return (groups + BM - 1) / BM; }
+__host__ __device__ __forceinline__ int col_tiles(int groups) { return (groups + BN - 1) / BN; }
 
-// One operand tile of one ring stage: 128 rows x 64 bf16 (128 B per row, no
-// padding).  Rows are XOR-swizzled in 16-byte chunks (physical chunk =
-// logical chunk ^ ((row / 2) % 8)) so that the 32x32 fragment reads of 16
-// consecutive rows hit 16 distinct bank groups.
-constexpr int STAGE_ELEMS = BM * BK;
-constexpr int NSTAGE = 4;     // ring depth: loads run NSTAGE - 1 stages ahead
+// One ring stage: the Q tile (BM rows) and the K tile (BN rows) of 64 bf16
+// each (128 B per row, no padding).  Rows are XOR-swizzled in 16-byte chunks
+// (physical chunk = logical chunk ^ ((row / 2) % 8)) so that the 32x32
+// fragment reads of 16 consecutive rows hit 16 distinct bank groups.
+constexpr int A_ELEMS = BM * BK;
+constexpr int B_ELEMS = BN * BK;
+constexpr int NSTAGE = 3;     // ring depth: loads run NSTAGE - 1 stages ahead
+constexpr int A_LOADS = BM / 8 / 4;   // 1 KB loads per wave per stage (8 rows each)
+constexpr int B_LOADS = BN / 8 / 4;
+constexpr int VM_STAGE = A_LOADS + B_LOADS;
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;
 constexpr int PT_MAX = 2048;  // page-table entries one tile of a paged cache may span
 constexpr uint32_t BAD_PAGE = 0xFFFFFFFFu;
@@ -105,14 +110,13 @@ __device__ __forceinline__ void dma16(i32x4 rs, uint32_t lds, uint32_t voff) {
 
 template <int G, bool PAGED>
 __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
-  // ring slot s: Q tile at ring[s][0], K tile at ring[s][1]
-  __shared__ __align__(1024) bf16_t ring[NSTAGE][2][STAGE_ELEMS];
+  // ring slot s: Q tile at ring[s][0 .. A_ELEMS), K tile after it
+  __shared__ __align__(1024) bf16_t ring[NSTAGE][A_ELEMS + B_ELEMS];
   __shared__ uint32_t page_base[PAGED ? PT_MAX : 1];  // byte offset of each page, or BAD_PAGE
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hi = lane >> 5;
-  const int wi = wave >> 1, wj = wave & 1;
 
   // ---- tile decode: (request, tile rank, head) with the KV head fastest ----
   const int ri = find_req(a.batch, blockIdx.x);
@@ -123,7 +127,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   const int local = blockIdx.x - R.work_begin;
   const int nqg = (n_q + a.g - 1) / a.g;    // query groups
   const int nkg = (n_kv + a.g - 1) / a.g;   // key groups
-  const int ntj = tiles_of(nkg);
+  const int ntj = col_tiles(nkg);
   const int h = local % a.h_kv;
   const int pm = (local / a.h_kv) % a.m;
   const int rank = local / a.h_q;
@@ -141,9 +145,9 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   }
 
   // ---- direct global -> LDS loads through buffer descriptors ----
-  // Wave w, load i (0..3) fills rows [8 (4 i + w), +8) of a stage: lane l
-  // writes LDS chunk l % 8 of row 8 (4 i + w) + l / 8 and fetches the
-  // logical chunk that the swizzle places there.  Out-of-range offsets
+  // Wave w, load i fills rows [8 (4 i + w), +8) of the Q (i < A_LOADS) or K
+  // (i < B_LOADS) tile: lane l writes LDS chunk l % 8 of row 8 (4 i + w) +
+  // l / 8 and fetches the logical chunk that the swizzle places there.  Out-of-range offsets
   // (padding groups, tokens past the end, bad pages) read as zeros.  The Q
   // descriptor starts at the tile's first query token, so it spans at most
   // BM * g token rows.
@@ -172,33 +176,38 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
     __syncthreads();
   }
   const int row_sub = lane >> 3, pch = lane & 7;
-  int q_row_tok[4], k_row_tok[4];   // first token of the group of each loaded row
-  int lch[4];                       // logical chunk fetched by this lane
-  bool q_ok[4], k_ok[4];
+  int q_row_tok[A_LOADS], k_row_tok[B_LOADS];   // first token of each loaded row's group
+  int lch[A_LOADS];                             // logical chunk fetched by this lane
+  bool q_ok[A_LOADS], k_ok[B_LOADS];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 8 * (4 * i + wave) + row_sub;
+  for (int i = 0; i < A_LOADS; ++i) {
+    const int row = 8 * (4 * i + wave) + row_sub;   // the K rows are the first B_LOADS of these
     lch[i] = swz(row, pch);
-    const int gi = ti * BM + row, gj = tj * BN + row;
-    q_ok[i] = gi < nqg;
-    k_ok[i] = gj < nkg;
+    q_ok[i] = ti * BM + row < nqg;
     q_row_tok[i] = row * a.g;   // relative to q_tok0
-    k_row_tok[i] = gj * a.g;
+    if (i < B_LOADS) {
+      const int gj = tj * BN + row;
+      k_ok[i] = gj < nkg;
+      k_row_tok[i] = gj * a.g;
+    }
   }
-  const uint32_t ring_lds = LDS_ADDR(&ring[0][0][0]) + (uint32_t)wave * 1024;
-  constexpr uint32_t SLOT_BYTES = 2 * STAGE_ELEMS * 2;
+  const uint32_t ring_lds = LDS_ADDR(&ring[0][0]) + (uint32_t)wave * 1024;
+  constexpr uint32_t SLOT_BYTES = (A_ELEMS + B_ELEMS) * 2;
   auto issue = [&](int st) __attribute__((always_inline)) {
     const uint32_t la = ring_lds + (uint32_t)(st % NSTAGE) * SLOT_BYTES;
-    const uint32_t lb = la + STAGE_ELEMS * 2;
+    const uint32_t lb = la + A_ELEMS * 2;
     const int k0 = st * BK;
     const int tok_in = k0 / a.C, ch = k0 % a.C;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < A_LOADS; ++i) {
       const int tq = q_row_tok[i] + tok_in;
       const uint32_t qo = (q_ok[i] && tq < q_tile_tok)
                               ? (uint32_t)(((int64_t)tq * a.q_st + ch + 8 * lch[i]) * 2)
                               : 0x80000000u;
       dma16(qrs, la + i * 4096, qo);
+    }
+#pragma unroll
+    for (int i = 0; i < B_LOADS; ++i) {
       const int tk = k_row_tok[i] + tok_in;
       uint32_t ko = 0x80000000u;
       if (k_ok[i] && tk < n_kv) {
@@ -215,11 +224,12 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
     }
   };
 
-  f32x16 acc[2][2], tot[2][2];
+  // wave w: query-group rows [64 w, +64) x all BN key-group columns
+  f32x16 acc[2][4], tot[2][4];
 #pragma unroll
   for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int y = 0; y < 2; ++y)
+    for (int y = 0; y < 4; ++y)
 #pragma unroll
       for (int r = 0; r < 16; ++r) { acc[x][y][r] = 0.f; tot[x][y][r] = 0.f; }
 
@@ -227,25 +237,26 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   auto compute = [&](const bf16_t* A, const bf16_t* B) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[2], bf[2];
+      bf16x8 af[2], bf[4];
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
-        const int row = 64 * wi + 32 * x + l32;
+        const int row = 64 * wave + 32 * x + l32;
         af[x] = __builtin_bit_cast(bf16x8, ld16(A + row * BK + 8 * swz(row, 2 * ks + hi)));
       }
 #pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const int row = 64 * wj + 32 * y + l32;
+      for (int y = 0; y < 4; ++y) {
+        const int row = 32 * y + l32;
         bf[y] = __builtin_bit_cast(bf16x8, ld16(B + row * BK + 8 * swz(row, 2 * ks + hi)));
       }
 #pragma unroll
       for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(af[x], bf[y], acc[x][y]);
+        for (int y = 0; y < 4; ++y) acc[x][y] = mfma32(af[x], bf[y], acc[x][y]);
     }
   };
   // s_waitcnt immediates: vmcnt(n) with the other counters left free
-  constexpr int VM16 = 0x4F70, VM8 = 0x0F78, VM0 = 0x0F70;
+  constexpr int VM_AHEAD = 0x0F70 | VM_STAGE, VM0 = 0x0F70;
+  static_assert(NSTAGE == 3 && VM_STAGE < 16, "one stage ahead, vmcnt below 16");
 
   // prologue: stages 0 .. NSTAGE - 2 in flight
   for (int st = 0; st < NSTAGE - 1 && st < n_stage; ++st) issue(st);
@@ -253,25 +264,23 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
     const int c1 = min(c0 + CHAIN, n_stage);
     for (int st = c0; st < c1; ++st) {
       // this wave's loads of stage st are done once at most the loads of the
-      // stages after it (up to NSTAGE - 2, 8 each) remain; the barrier then
-      // makes every wave's part visible, and also tells that every wave is
-      // done reading the slot refilled next (stage st - 1's)
-      const int ahead = min(NSTAGE - 2, n_stage - 1 - st);
-      if (ahead == 2) __builtin_amdgcn_s_waitcnt(VM16);
-      else if (ahead == 1) __builtin_amdgcn_s_waitcnt(VM8);
+      // stage after it (VM_STAGE) remain; the barrier then makes every wave's
+      // part visible, and also tells that every wave is done reading the slot
+      // refilled next (stage st - 1's)
+      if (st + 1 < n_stage) __builtin_amdgcn_s_waitcnt(VM_AHEAD);
       else __builtin_amdgcn_s_waitcnt(VM0);
       // plain barrier: a __syncthreads() fence would also wait for the
       // loads still in flight for the later stages
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
       if (st + NSTAGE - 1 < n_stage) issue(st + NSTAGE - 1);
       const int slot = st % NSTAGE;
-      compute(&ring[slot][0][0], &ring[slot][1][0]);
+      compute(&ring[slot][0], &ring[slot][A_ELEMS]);
     }
     // close the chain: fold it into the running total
 #pragma unroll
     for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int y = 0; y < 2; ++y)
+      for (int y = 0; y < 4; ++y)
 #pragma unroll
         for (int r = 0; r < 16; ++r) { tot[x][y][r] += acc[x][y][r]; acc[x][y][r] = 0.f; }
   }
@@ -282,12 +291,12 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
 #pragma unroll
   for (int x = 0; x < 2; ++x) {
 #pragma unroll
-    for (int y = 0; y < 2; ++y) {
-      const int gj = tj * BN + 64 * wj + 32 * y + l32;
+    for (int y = 0; y < 4; ++y) {
+      const int gj = tj * BN + 32 * y + l32;
       f32x16 v = tot[x][y];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int gi = ti * BM + 64 * wi + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
+        const int gi = ti * BM + 64 * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
         if (gi >= nqg || gj >= nkg) v[r] = -INFINITY;
       }
       // pool over G consecutive query-group rows
@@ -323,7 +332,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
       if (j >= R.l_kv) continue;
 #pragma unroll
       for (int r = 0; r < 16; r += (G >= 16 ? 8 : G >= 4 ? 4 : G)) {
-        const int gi = ti * BM + 64 * wi + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
+        const int gi = ti * BM + 64 * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
         const int i = gi / G;
         if (i >= R.l_q) continue;
         const int e_i = min(n_c + (i + 1) * a.b - 1, R.n_kv - 1);
@@ -453,7 +462,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
     if (d.l_kv > MAX_LKV) return hipErrorInvalidValue;
     d.work_begin = n_tiles;
     const int nqg = (d.n_q + a.g - 1) / a.g, nkg = (d.n_kv + a.g - 1) / a.g;
-    n_tiles += a.h_q * tiles_of(nqg) * tiles_of(nkg);
+    n_tiles += a.h_q * row_tiles(nqg) * col_tiles(nkg);
   }
   hipError_t e;
   switch (a.G) {
