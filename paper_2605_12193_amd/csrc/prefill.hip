@@ -26,10 +26,15 @@
 //
 // The lane ^ 32 exchanges of the row max and sum use v_permlane32_swap.
 //
-// The online softmax keeps a stale running max: O and l are rescaled only
-// when a row's max grows by more than 2^RESCALE_LOG2 in the exp2 domain.
-// Both are always scaled by the same max, so O / l is exact, and every
-// weight stays <= 2^RESCALE_LOG2.
+// The online softmax keeps a stale running max and takes no max reduction in
+// the common case: a tile's weights are computed against the running max and
+// kept when every row's weight sum over the tile is <= 2^RESCALE_LOG2 (so is
+// every weight).  Otherwise, and on a row's first tile, the tile's max is
+// taken, the running max moves up to it where it is larger (O and l
+// rescaled) and the weights are recomputed (all <= 1).  O and l always refer
+// to the same max, so O / l is exact.
+#include <utility>
+
 #include "bfla_device.h"
 #include "bfla_internal.h"
 
@@ -39,6 +44,7 @@ namespace {
 constexpr int TILE = 64;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float RESCALE_LOG2 = 8.0f;
+constexpr float RESCALE_SUM = 256.0f;      // 2^RESCALE_LOG2
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;  // raw buffer, 32-bit data format
 constexpr int VMCNT0 = 0x0F70;                // s_waitcnt vmcnt(0), other counters free
 
@@ -127,20 +133,36 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off)
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
 
-// Scheduling pins for an MFMA stream fed from LDS: the first DEPTH operand
-// reads, then alternating (MFMA, read) pairs, then the last DEPTH MFMAs.
-// Without them the scheduler keeps only ~2 reads in flight and every MFMA
-// waits on the LDS latency.
-constexpr int SG_MFMA = 0x008, SG_DS_READ = 0x100;
-template <int DEPTH, int N>
-__device__ __forceinline__ void pin_read_ahead() {
-  __builtin_amdgcn_sched_group_barrier(SG_DS_READ, DEPTH, 0);
-#pragma unroll
-  for (int j = 0; j < N - DEPTH; ++j) {
-    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
-  }
-  __builtin_amdgcn_sched_group_barrier(SG_MFMA, DEPTH, 0);
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+#define LDS_ADDR(arr) ((uint32_t)(uintptr_t)(lds_ptr_t)(arr))
+
+// f(std::integral_constant<int, 0>) ... f(std::integral_constant<int, N - 1>),
+// so that the body can use its index as a constant (immediate operands).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_seq(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// 16-byte LDS read issued exactly where it stands.  The result is in flight
+// until a later lgkm_wait on the same value; the compiler does not track it.
+template <int OFF>
+__device__ __forceinline__ void lds_read(u32x4& r, uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds_read offset field is 16 bits");
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF) : "memory");
+}
+// Wait until at most N LDS/scalar-memory operations are outstanding.  r is an
+// in/out operand so that no use of r can move above the wait.  LDS operations
+// complete in issue order, so waiting for N leaves only the last N reads
+// pending; other LDS or scalar loads in flight can only make it stricter.
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u32x4& r) {
+  static_assert(N >= 0 && N < 16, "lgkmcnt field is 4 bits");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(r) : "i"(N));
 }
 
 // Shapes whose 2m-wave workgroup would cap registers below what the loop
@@ -348,6 +370,7 @@ prefill_kernel(PrefillArgs a) {
   const float c2 = a.scale * LOG2E;
   float m_run = -INFINITY;   // stale running max of the raw scores
   float l_run = 0.f;
+  bool max_ok = false;       // every lane of the wave has a finite m_run
   f32x16 acc[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb)
@@ -357,31 +380,82 @@ prefill_kernel(PrefillArgs a) {
   auto tile_at = [&](int i) -> int { return DENSE ? i : uniform_load(a.cols, list_begin + i); };
   auto stage = [&](int slot) -> bf16_t* { return lds + slot * CF::STAGE; };
 
-  // S^T = K . Q^T  (two 32-key blocks) from the K tile of one stage.  The
-  // LDS operand reads run DEPTH fragments ahead of the MFMAs that use them.
+  // ---- MFMA streams fed from LDS ----
+  // S^T = K . Q^T (two 32-key blocks, Q held in registers) and
+  // O^T += V^T . P^T (channel block fastest, so consecutive MFMAs accumulate
+  // into different registers).  One stream runs the PV product of one tile
+  // and/or the QK product of another.  Its operand fragments are read
+  // DEPTH ahead in exactly the order the MFMAs consume them, with the waits
+  // placed by hand: left to the scheduler, the reads of a ring get reordered
+  // and every few MFMAs wait on a read issued just before them.
   constexpr int DEPTH = 4;
+  const uint32_t lds_base = LDS_ADDR(lds);
+  const uint32_t k_lane = lds_base + (uint32_t)((l32 * CF::KROW + 8 * hi) * 2);
+  const uint32_t v_lane = lds_base + (uint32_t)((CF::K_ELEMS + l32 * CF::VROW + 8 * hi) * 2);
   f32x16 s0, s1;
-  auto k_frag = [&](const bf16_t* ks, int j) -> bf16x8 {   // j = 2 kc + block
-    return as_bf16x8(ld16(ks + ((j & 1) * 32 + l32) * CF::KROW + 16 * (j >> 1) + 8 * hi));
+  bf16x8 pf[4];   // P^T of the tile being multiplied by V
+  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot) {
+    constexpr int NV = decltype(do_pv)::value ? 4 * NCB : 0;   // V^T fragments
+    constexpr int NK = decltype(do_qk)::value ? 2 * NKC : 0;   // K fragments
+    constexpr int N = NV + NK;
+    const uint32_t va = v_lane + (uint32_t)(v_slot * CF::STAGE * 2);
+    const uint32_t ka = k_lane + (uint32_t)(k_slot * CF::STAGE * 2);
+    u32x4 ring[DEPTH];
+    // fragment j < NV: V^T rows 32 (j % NCB).., keys 16 (j / NCB)..;
+    // else j' = j - NV: K rows 32 (j' % 2).., channels 16 (j' / 2)..
+    auto issue = [&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j < NV)
+        lds_read<(32 * (j % NCB) * CF::VROW + 16 * (j / NCB)) * 2>(ring[j % DEPTH], va);
+      else
+        lds_read<(((j - NV) & 1) * 32 * CF::KROW + 16 * ((j - NV) >> 1)) * 2>(ring[j % DEPTH], ka);
+    };
+    static_for<(DEPTH < N ? DEPTH : N)>(issue);
+    const f32x16 zero = {};
+    static_for<N>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      // reads issued after fragment j so far: min(N, DEPTH + j) - j - 1
+      lgkm_wait<(N - 1 - j < DEPTH - 1 ? N - 1 - j : DEPTH - 1)>(ring[j % DEPTH]);
+      const bf16x8 a = __builtin_bit_cast(bf16x8, ring[j % DEPTH]);
+      if constexpr (j < NV) {
+        acc[j % NCB] = mfma32(a, pf[j / NCB], acc[j % NCB]);
+      } else if constexpr (((j - NV) & 1) != 0) {
+        s1 = mfma32(a, qf[(j - NV) >> 1], j - NV < 2 ? zero : s1);   // S starts at 0
+      } else {
+        s0 = mfma32(a, qf[(j - NV) >> 1], j - NV < 2 ? zero : s0);
+      }
+      if constexpr (j + DEPTH < N) issue(std::integral_constant<int, j + DEPTH>{});
+      // keep every MFMA between its own wait and the next read (the 2-stage
+      // shapes stage whole tiles through registers and need the scheduler's
+      // freedom to fit them)
+      if constexpr (PP) __builtin_amdgcn_sched_barrier(0);
+    });
   };
-  auto qk = [&](const bf16_t* ks) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) { s0[r] = 0.f; s1[r] = 0.f; }
-    bf16x8 ring[DEPTH];
-#pragma unroll
-    for (int j = 0; j < DEPTH; ++j) ring[j] = k_frag(ks, j);
-#pragma unroll
-    for (int j = 0; j < 2 * NKC; ++j) {
-      const bf16x8 a = ring[j % DEPTH];
-      if (j + DEPTH < 2 * NKC) ring[j % DEPTH] = k_frag(ks, j + DEPTH);
-      if (j & 1) s1 = mfma32(a, qf[j >> 1], s1);
-      else s0 = mfma32(a, qf[j >> 1], s0);
-    }
-    pin_read_ahead<DEPTH, 2 * NKC>();
-  };
+  const std::true_type YES;
+  const std::false_type NO;
 
   // online softmax of the scores of KV tile kt -> bf16 P^T operands
-  bf16x8 pf[4];
+  // P = exp2(S c2 + moff) as bf16 B operands (16-key chunk q = regs 8(q%2)..
+  // of block q/2); returns this lane's fp32 sum of the weights.
+  auto exp_pack = [&](float moff) -> float {
+    float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const f32x16& sb = (qq < 2) ? s0 : s1;
+      const int base = 8 * (qq & 1);
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(sb[base + 2 * e], c2, moff));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(sb[base + 2 * e + 1], c2, moff));
+        w[e] = pack_bf16x2(p0, p1);
+        r0 += p0;
+        r1 += p1;
+      }
+      pf[qq] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+    }
+    return r0 + r1;
+  };
   auto softmax = [&](int kt_s) {
     // token-level causal mask and key bound, only on tiles that need it; a
     // list entry outside [0, T_kv) contributes nothing
@@ -395,65 +469,35 @@ prefill_kernel(PrefillArgs a) {
         s1[r] = kk + 32 <= lim ? s1[r] : -INFINITY;
       }
     }
-    // row max over this lane's 32 keys: a chain of 3-input max
-    float mx = fmaxf(s0[0], s1[0]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);
-    mx = max_lane32(mx);
-    // move the stale max only when the new max exceeds it by 2^RESCALE_LOG2
-    const bool grow = (mx - m_run) * c2 > RESCALE_LOG2 || (m_run == -INFINITY && mx != -INFINITY);
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      const float m_new = grow ? mx : m_run;
-      const float corr = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c2) : 1.f;
-      m_run = m_new;
-      l_run *= corr;
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[cb][r] *= corr;
+    // Common case: weights against the stale max, accepted when the row's
+    // weight sum for this tile stays <= 2^RESCALE_LOG2 (so does every weight).
+    bool done = false;
+    float rs = 0.f;
+    if (max_ok) {
+      rs = add_lane32(exp_pack(-m_run * c2));
+      done = !__builtin_amdgcn_ballot_w64(!(rs <= RESCALE_SUM));
     }
-    const float moff = (m_run == -INFINITY) ? 0.f : -m_run * c2;
-    float rs0 = 0.f, rs1 = 0.f;
+    if (!done) {
+      // row max over this lane's 32 keys: a chain of 3-input max
+      float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], c2, moff));
-      s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], c2, moff));
-      rs0 += s0[r];
-      rs1 += s1[r];
+      for (int r = 1; r < 16; ++r) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);
+      mx = max_lane32(mx);
+      const bool grow = mx > m_run;
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float corr = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c2) : 1.f;
+        m_run = m_new;
+        l_run *= corr;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[cb][r] *= corr;
+      }
+      max_ok = !__builtin_amdgcn_ballot_w64(m_run == -INFINITY);
+      rs = add_lane32(exp_pack((m_run == -INFINITY) ? 0.f : -m_run * c2));
     }
-    const float rs = add_lane32(rs0 + rs1);
     l_run += rs;
-    // P^T (bf16) as B operands: 16-key chunk q = regs 8(q%2).. of block q/2
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      const f32x16& sb = (qq < 2) ? s0 : s1;
-      const int base = 8 * (qq & 1);
-      uint4 u;
-      u.x = pack_bf16x2(sb[base + 0], sb[base + 1]);
-      u.y = pack_bf16x2(sb[base + 2], sb[base + 3]);
-      u.z = pack_bf16x2(sb[base + 4], sb[base + 5]);
-      u.w = pack_bf16x2(sb[base + 6], sb[base + 7]);
-      pf[qq] = as_bf16x8(u);
-    }
-  };
-
-  // O^T += V^T . P^T from the V^T tile of one stage (same read-ahead ring).
-  // The channel block varies fastest, so consecutive MFMAs accumulate into
-  // different registers.
-  auto v_frag = [&](const bf16_t* vs, int j) -> bf16x8 {   // j = NCB q + cb
-    return as_bf16x8(ld16(vs + (32 * (j % NCB) + l32) * CF::VROW + 16 * (j / NCB) + 8 * hi));
-  };
-  auto pv = [&](const bf16_t* vs) {
-    bf16x8 ring[DEPTH];
-#pragma unroll
-    for (int j = 0; j < DEPTH; ++j) ring[j] = v_frag(vs, j);
-#pragma unroll
-    for (int j = 0; j < 4 * NCB; ++j) {
-      const bf16x8 a = ring[j % DEPTH];
-      if (j + DEPTH < 4 * NCB) ring[j % DEPTH] = v_frag(vs, j + DEPTH);
-      acc[j % NCB] = mfma32(a, pf[j / NCB], acc[j % NCB]);
-    }
-    pin_read_ahead<DEPTH, 4 * NCB>();
   };
 
   if (PP) {
@@ -461,9 +505,11 @@ prefill_kernel(PrefillArgs a) {
     // an iteration ahead of group B (waves 4-7); each SIMD hosts one wave of
     // each group, so in every phase one of them issues MFMAs while the other
     // runs the softmax.  Tile i lives in stage i % 3.
-    //   phase X_i: A softmax(i)            | B PV(i-1), QK(i)
-    //   phase Y_i: A PV(i), QK(i+1)        | B softmax(i); all: store tile i+2
-    // Stage (i+2) % 3 == (i-1) % 3 is last read by B in phase X_i.
+    //   phase Y_i:   A PV(i), QK(i+1)      | B softmax(i); all: store tile i+2
+    //   phase X_i+1: A softmax(i+1)        | B PV(i), QK(i+1)
+    // Stage (i+2) % 3 == (i-1) % 3 is last read by B in phase X_i.  Each
+    // group runs one PV+QK stream per iteration; the QK of the last one reads
+    // a stage no one writes any more and its scores are never used.
     const bool grp_a = ((wave >> 2) & 1) == 0;
     int kt_i = 0, kt_i1 = 0, kt_i2 = 0, kt_i3 = 0;  // tiles i .. i+3
     if (n_tiles > 0) kt_i = tile_at(0);
@@ -474,27 +520,21 @@ prefill_kernel(PrefillArgs a) {
     if (n_tiles > 1) { load_tile(kt_i1); store_tile(stage(1)); }
     if (n_tiles > 2) load_tile(kt_i2);
     __syncthreads();
-    if (grp_a && n_tiles > 0) qk(stage(0));
-    __syncthreads();
+    if (n_tiles > 0) {
+      if (grp_a) stream(NO, YES, 0, 0);
+      __syncthreads();
+      // phase X_0
+      if (grp_a) softmax(kt_i);
+      else stream(NO, YES, 0, 0);
+      __syncthreads();
+    }
     int slot = 0;  // i % 3
     for (int it = 0; it < n_tiles; ++it) {
       const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
       const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
-      // phase X
-      if (grp_a) {
-        softmax(kt_i);
-      } else {
-        if (it > 0) pv(stage(slot2) + CF::K_ELEMS);
-        qk(stage(slot));
-      }
-      __syncthreads();
-      // phase Y
-      if (grp_a) {
-        pv(stage(slot) + CF::K_ELEMS);
-        if (it + 1 < n_tiles) qk(stage(slot1));
-      } else {
-        softmax(kt_i);
-      }
+      // phase Y_i
+      if (grp_a) stream(YES, YES, slot, slot1);
+      else softmax(kt_i);
       if (it + 2 < n_tiles) {
         store_tile(stage(slot2));
         if (it + 3 < n_tiles) load_tile(kt_i3);
@@ -503,10 +543,13 @@ prefill_kernel(PrefillArgs a) {
       kt_i1 = kt_i2;
       kt_i2 = kt_i3;
       if (it + 4 < n_tiles) kt_i3 = tile_at(it + 4);
+      __syncthreads();
+      // phase X_i+1
+      if (!grp_a) stream(YES, YES, slot, slot1);
+      else if (it + 1 < n_tiles) softmax(kt_i);
       slot = slot1;
       __syncthreads();
     }
-    if (!grp_a && n_tiles > 0) pv(stage(slot == 0 ? 2 : slot - 1) + CF::K_ELEMS);
   } else {
     // Two LDS stages, every wave in the same phase: the next list entry's
     // tile is fetched into registers while the current one is consumed.
@@ -526,10 +569,9 @@ prefill_kernel(PrefillArgs a) {
         kt = kt_next;
         if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
       }
-      const bf16_t* ks = stage(it & 1);
-      qk(ks);
+      stream(NO, YES, 0, it & 1);
       softmax(kt_cur);
-      pv(ks + CF::K_ELEMS);
+      stream(YES, NO, it & 1, 0);
       if (more) store_tile(stage((it + 1) & 1));
       __syncthreads();
     }
