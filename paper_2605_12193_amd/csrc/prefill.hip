@@ -133,6 +133,10 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off)
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
 
+// every lambda of the kernel body is inlined (the loop calls some of them
+// from several places, which the inliner would otherwise turn into calls)
+#define INLINE __attribute__((always_inline))
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 #define LDS_ADDR(arr) ((uint32_t)(uintptr_t)(lds_ptr_t)(arr))
@@ -286,12 +290,15 @@ prefill_kernel(PrefillArgs a) {
   const uint32_t tile_bytes = (uint32_t)(TILE * st * 2);
   const uint32_t st_bytes = (uint32_t)(st * 2);
 
-  uint4 kreg[KC_PER_T];
-  uint4 vreg[VU_PER_T][2];
+  // one K/V tile on its way from memory to LDS, in registers
+  struct Staged {
+    uint4 k[KC_PER_T];
+    uint4 v[VU_PER_T][2];
+  };
 
   // Byte offset of (key, 8-channel chunk ce) in a paged pool, given the page
   // numbers of the tile's (up to 4) pages read as scalars.
-  auto paged_off = [&](int tok0, int kr, int ce, const int* pg) -> uint32_t {
+  auto paged_off = [&](int tok0, int kr, int ce, const int* pg) INLINE -> uint32_t {
     const int key = tok0 + kr;
     if (key >= n_kv) return 0x80000000u;
     const int slot = ps >= TILE ? 0 : (kr >> ps_shift);
@@ -299,7 +306,7 @@ prefill_kernel(PrefillArgs a) {
     return (uint32_t)page * page_bytes + (uint32_t)(((key & (ps - 1)) * st + 8 * ce) * 2);
   };
 
-  auto load_tile = [&](int kt) {
+  auto load_tile = [&](int kt, Staged& sg) INLINE {
     // tiles outside [0, T_kv) (malformed lists) load nothing
     const bool ok = (unsigned)kt < (unsigned)t_kv;
     if (!PAGED) {
@@ -308,12 +315,12 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
         if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-          kreg[i] = bload16(krs, base + k_boff[i]);
+          sg.k[i] = bload16(krs, base + k_boff[i]);
 #pragma unroll
       for (int i = 0; i < VU_PER_T; ++i)
         if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-          vreg[i][0] = bload16(vrs, base + v_boff[i]);
-          vreg[i][1] = bload16(vrs, base + v_boff[i] + st_bytes);
+          sg.v[i][0] = bload16(vrs, base + v_boff[i]);
+          sg.v[i][1] = bload16(vrs, base + v_boff[i] + st_bytes);
         }
       return;
     }
@@ -330,29 +337,29 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
       if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-        kreg[i] = bload16(krs, paged_off(tok0, k_row[i], k_ce[i], pg));
+        sg.k[i] = bload16(krs, paged_off(tok0, k_row[i], k_ce[i], pg));
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-        vreg[i][0] = bload16(vrs, paged_off(tok0, 2 * v_j[i], v_ce[i], pg));
-        vreg[i][1] = bload16(vrs, paged_off(tok0, 2 * v_j[i] + 1, v_ce[i], pg));
+        sg.v[i][0] = bload16(vrs, paged_off(tok0, 2 * v_j[i], v_ce[i], pg));
+        sg.v[i][1] = bload16(vrs, paged_off(tok0, 2 * v_j[i] + 1, v_ce[i], pg));
       }
   };
 
-  auto store_tile = [&](bf16_t* stg) {
+  auto store_tile = [&](bf16_t* stg, const Staged& sg) INLINE {
     bf16_t* ks = stg;
     bf16_t* vs = stg + CF::K_ELEMS;
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i) {
       if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-        *reinterpret_cast<uint4*>(ks + k_row[i] * CF::KROW + 8 * k_ce[i]) = kreg[i];
+        *reinterpret_cast<uint4*>(ks + k_row[i] * CF::KROW + 8 * k_ce[i]) = sg.k[i];
     }
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i) {
       if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
         const int pos = vperm(2 * v_j[i]);
-        const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-        const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
+        const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
+        const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
         bf16_t* col = vs + 8 * v_ce[i] * CF::VROW + pos;
 #pragma unroll
         for (int e2 = 0; e2 < 4; ++e2) {
@@ -377,8 +384,12 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
-  auto tile_at = [&](int i) -> int { return DENSE ? i : uniform_load(a.cols, list_begin + i); };
-  auto stage = [&](int slot) -> bf16_t* { return lds + slot * CF::STAGE; };
+  // (the index is made explicitly uniform: inside the unrolled ping-pong loop
+  // the compiler no longer proves it so and would emit a vector load)
+  auto tile_at = [&](int i) INLINE -> int {
+    return DENSE ? i : uniform_load(a.cols, __builtin_amdgcn_readfirstlane(list_begin + i));
+  };
+  auto stage = [&](int slot) INLINE -> bf16_t* { return lds + slot * CF::STAGE; };
 
   // ---- MFMA streams fed from LDS ----
   // S^T = K . Q^T (two 32-key blocks, Q held in registers) and
@@ -394,7 +405,7 @@ prefill_kernel(PrefillArgs a) {
   const uint32_t v_lane = lds_base + (uint32_t)((CF::K_ELEMS + l32 * CF::VROW + 8 * hi) * 2);
   f32x16 s0, s1;
   bf16x8 pf[4];   // P^T of the tile being multiplied by V
-  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot) {
+  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot) INLINE {
     constexpr int NV = decltype(do_pv)::value ? 4 * NCB : 0;   // V^T fragments
     constexpr int NK = decltype(do_qk)::value ? 2 * NKC : 0;   // K fragments
     constexpr int N = NV + NK;
@@ -403,7 +414,7 @@ prefill_kernel(PrefillArgs a) {
     u32x4 ring[DEPTH];
     // fragment j < NV: V^T rows 32 (j % NCB).., keys 16 (j / NCB)..;
     // else j' = j - NV: K rows 32 (j' % 2).., channels 16 (j' / 2)..
-    auto issue = [&](auto jc) {
+    auto issue = [&](auto jc) INLINE {
       constexpr int j = decltype(jc)::value;
       if constexpr (j < NV)
         lds_read<(32 * (j % NCB) * CF::VROW + 16 * (j / NCB)) * 2>(ring[j % DEPTH], va);
@@ -437,7 +448,7 @@ prefill_kernel(PrefillArgs a) {
   // online softmax of the scores of KV tile kt -> bf16 P^T operands
   // P = exp2(S c2 + moff) as bf16 B operands (16-key chunk q = regs 8(q%2)..
   // of block q/2); returns this lane's fp32 sum of the weights.
-  auto exp_pack = [&](float moff) -> float {
+  auto exp_pack = [&](float moff) INLINE -> float {
     float r0 = 0.f, r1 = 0.f;
 #pragma unroll
     for (int qq = 0; qq < 4; ++qq) {
@@ -456,7 +467,7 @@ prefill_kernel(PrefillArgs a) {
     }
     return r0 + r1;
   };
-  auto softmax = [&](int kt_s) {
+  auto softmax = [&](int kt_s) INLINE {
     // token-level causal mask and key bound, only on tiles that need it; a
     // list entry outside [0, T_kv) contributes nothing
     const int key0 = kt_s * TILE;
@@ -510,53 +521,73 @@ prefill_kernel(PrefillArgs a) {
     // Stage (i+2) % 3 == (i-1) % 3 is last read by B in phase X_i.  Each
     // group runs one PV+QK stream per iteration; the QK of the last one reads
     // a stage no one writes any more and its scores are never used.
+    //   Tile i + 4 is fetched into registers in phase Y_i and stored in
+    // Y_i+2: two register sets, the loop unrolled by two so each is fixed.
+    // Past the end of the list the loads read zeros (no memory traffic) and
+    // the stores fill a stage no one reads, so the loop body has no branches
+    // around its memory operations.
     const bool grp_a = ((wave >> 2) & 1) == 0;
-    int kt_i = 0, kt_i1 = 0, kt_i2 = 0, kt_i3 = 0;  // tiles i .. i+3
-    if (n_tiles > 0) kt_i = tile_at(0);
-    if (n_tiles > 1) kt_i1 = tile_at(1);
-    if (n_tiles > 2) kt_i2 = tile_at(2);
-    if (n_tiles > 3) kt_i3 = tile_at(3);
-    if (n_tiles > 0) { load_tile(kt_i); store_tile(stage(0)); }
-    if (n_tiles > 1) { load_tile(kt_i1); store_tile(stage(1)); }
-    if (n_tiles > 2) load_tile(kt_i2);
-    __syncthreads();
+    // the list read itself is unconditional (index clamped) so that it stays
+    // a scalar load: a vector load would share vmcnt with the K/V prefetch
+    auto tile_or_none = [&](int i) INLINE -> int {
+      const int t = tile_at(min(i, n_tiles - 1));
+      return i < n_tiles ? t : -1;
+    };
     if (n_tiles > 0) {
+      Staged sg0, sg1;
+      int kt[5];  // tiles i .. i+4
+#pragma unroll
+      for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
+      load_tile(kt[0], sg0);
+      load_tile(kt[1], sg1);
+      store_tile(stage(0), sg0);
+      store_tile(stage(1), sg1);
+      load_tile(kt[2], sg0);
+      load_tile(kt[3], sg1);
+      __syncthreads();
       if (grp_a) stream(NO, YES, 0, 0);
       __syncthreads();
       // phase X_0
-      if (grp_a) softmax(kt_i);
+      if (grp_a) softmax(kt[0]);
       else stream(NO, YES, 0, 0);
       __syncthreads();
-    }
-    int slot = 0;  // i % 3
-    for (int it = 0; it < n_tiles; ++it) {
-      const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
-      const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
-      // phase Y_i
-      if (grp_a) stream(YES, YES, slot, slot1);
-      else softmax(kt_i);
-      if (it + 2 < n_tiles) {
-        store_tile(stage(slot2));
-        if (it + 3 < n_tiles) load_tile(kt_i3);
+      int slot = 0;  // i % 3
+      int it = 0;
+      // one iteration: phases Y_i and X_i+1, staging through sg
+      auto iteration = [&](Staged& sg) INLINE {
+        const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
+        const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
+        // phase Y_i
+        if (grp_a) stream(YES, YES, slot, slot1);
+        else softmax(kt[0]);
+        store_tile(stage(slot2), sg);   // tile i + 2
+        load_tile(kt[4], sg);           // tile i + 4
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
+        kt[4] = tile_or_none(it + 5);
+        __syncthreads();
+        // phase X_i+1
+        if (!grp_a) stream(YES, YES, slot, slot1);
+        else if (it + 1 < n_tiles) softmax(kt[0]);
+        slot = slot1;
+        __syncthreads();
+      };
+      for (; it + 1 < n_tiles; it += 2) {
+        iteration(sg0);
+        ++it;
+        iteration(sg1);
+        --it;
       }
-      kt_i = kt_i1;
-      kt_i1 = kt_i2;
-      kt_i2 = kt_i3;
-      if (it + 4 < n_tiles) kt_i3 = tile_at(it + 4);
-      __syncthreads();
-      // phase X_i+1
-      if (!grp_a) stream(YES, YES, slot, slot1);
-      else if (it + 1 < n_tiles) softmax(kt_i);
-      slot = slot1;
-      __syncthreads();
+      if (it < n_tiles) iteration(sg0);
     }
   } else {
     // Two LDS stages, every wave in the same phase: the next list entry's
     // tile is fetched into registers while the current one is consumed.
+    Staged sg;
     int kt_next = 0;
     if (n_tiles > 0) {
-      load_tile(tile_at(0));
-      store_tile(stage(0));
+      load_tile(tile_at(0), sg);
+      store_tile(stage(0), sg);
       if (n_tiles > 1) kt_next = tile_at(1);
     }
     __syncthreads();
@@ -565,14 +596,14 @@ prefill_kernel(PrefillArgs a) {
       const bool more = it + 1 < n_tiles;
       const int kt_cur = kt;
       if (more) {
-        load_tile(kt_next);
+        load_tile(kt_next, sg);
         kt = kt_next;
         if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
       }
       stream(NO, YES, 0, it & 1);
       softmax(kt_cur);
       stream(YES, NO, it & 1, 0);
-      if (more) store_tile(stage((it + 1) & 1));
+      if (more) store_tile(stage((it + 1) & 1), sg);
       __syncthreads();
     }
   }
