@@ -346,31 +346,33 @@ prefill_kernel(PrefillArgs a) {
       }
   };
 
-  auto store_tile = [&](bf16_t* stg, const Staged& sg) INLINE {
-    bf16_t* ks = stg;
-    bf16_t* vs = stg + CF::K_ELEMS;
+  // The staging stores of one thread, as pieces that can be placed apart:
+  // K chunk i, and V unit i (two keys x 8 channels, transposed on the way).
+  auto store_k = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+      *reinterpret_cast<uint4*>(stg + k_row[i] * CF::KROW + 8 * k_ce[i]) = sg.k[i];
+  };
+  auto store_v = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+      const int pos = vperm(2 * v_j[i]);
+      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
+      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
+      bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce[i] * CF::VROW + pos;
 #pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) {
-      if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-        *reinterpret_cast<uint4*>(ks + k_row[i] * CF::KROW + 8 * k_ce[i]) = sg.k[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VU_PER_T; ++i) {
-      if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-        const int pos = vperm(2 * v_j[i]);
-        const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
-        const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
-        bf16_t* col = vs + 8 * v_ce[i] * CF::VROW + pos;
-#pragma unroll
-        for (int e2 = 0; e2 < 4; ++e2) {
-          // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
-          const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
-          const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
-          *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
-          *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
-        }
+      for (int e2 = 0; e2 < 4; ++e2) {
+        // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
+        const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
+        const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
+        *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
+        *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
       }
     }
+  };
+  auto store_tile = [&](bf16_t* stg, const Staged& sg) INLINE {
+#pragma unroll
+    for (int i = 0; i < KC_PER_T; ++i) store_k(stg, sg, i);
+#pragma unroll
+    for (int i = 0; i < VU_PER_T; ++i) store_v(stg, sg, i);
   };
 
   // ---- online softmax state (one query per lane; both lane halves agree) ----
@@ -405,7 +407,10 @@ prefill_kernel(PrefillArgs a) {
   const uint32_t v_lane = lds_base + (uint32_t)((CF::K_ELEMS + l32 * CF::VROW + 8 * hi) * 2);
   f32x16 s0, s1;
   bf16x8 pf[4];   // P^T of the tile being multiplied by V
-  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot) INLINE {
+  auto no_hook = [](auto) INLINE {};
+  // hook(step) runs after the read of each step: other work placed between
+  // the MFMAs of the stream
+  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot, auto&& hook) INLINE {
     constexpr int NV = decltype(do_pv)::value ? 4 * NCB : 0;   // V^T fragments
     constexpr int NK = decltype(do_qk)::value ? 2 * NKC : 0;   // K fragments
     constexpr int N = NV + NK;
@@ -436,6 +441,7 @@ prefill_kernel(PrefillArgs a) {
         s0 = mfma32(a, qf[(j - NV) >> 1], j - NV < 2 ? zero : s0);
       }
       if constexpr (j + DEPTH < N) issue(std::integral_constant<int, j + DEPTH>{});
+      hook(jc);
       // keep every MFMA between its own wait and the next read (the 2-stage
       // shapes stage whole tiles through registers and need the scheduler's
       // freedom to fit them)
@@ -526,7 +532,6 @@ prefill_kernel(PrefillArgs a) {
     // Past the end of the list the loads read zeros (no memory traffic) and
     // the stores fill a stage no one reads, so the loop body has no branches
     // around its memory operations.
-    const bool grp_a = ((wave >> 2) & 1) == 0;
     // the list read itself is unconditional (index clamped) so that it stays
     // a scalar load: a vector load would share vmcnt with the K/V prefetch
     auto tile_or_none = [&](int i) INLINE -> int {
@@ -545,40 +550,59 @@ prefill_kernel(PrefillArgs a) {
       load_tile(kt[2], sg0);
       load_tile(kt[3], sg1);
       __syncthreads();
-      if (grp_a) stream(NO, YES, 0, 0);
-      __syncthreads();
-      // phase X_0
-      if (grp_a) softmax(kt[0]);
-      else stream(NO, YES, 0, 0);
-      __syncthreads();
-      int slot = 0;  // i % 3
-      int it = 0;
-      // one iteration: phases Y_i and X_i+1, staging through sg
-      auto iteration = [&](Staged& sg) INLINE {
-        const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
-        const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
-        // phase Y_i
-        if (grp_a) stream(YES, YES, slot, slot1);
-        else softmax(kt[0]);
-        store_tile(stage(slot2), sg);   // tile i + 2
-        load_tile(kt[4], sg);           // tile i + 4
+      // Each group runs its own copy of the loop (same barriers in the same
+      // order), so that the compiler sees one group's loads and stores as
+      // straight-line code and waits for exactly the older register set.
+      auto run = [&](auto is_a) INLINE {
+        constexpr bool A = decltype(is_a)::value;
+        // phase X_0 (A starts half an iteration ahead with QK(0))
+        if (A) stream(NO, YES, 0, 0, no_hook);
+        __syncthreads();
+        if (A) softmax(kt[0]);
+        else stream(NO, YES, 0, 0, no_hook);
+        __syncthreads();
+        int slot = 0;  // i % 3
+        int it = 0;
+        // one iteration: phases Y_i and X_i+1, staging through sg
+        auto iteration = [&](Staged& sg) INLINE {
+          const int slot1 = slot == 2 ? 0 : slot + 1;   // (i + 1) % 3
+          const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
+          bf16_t* const dst = stage(slot2);
+          const int kt_load = kt[4];
+          // the group stages its own part of tile i + 2 (into the free stage)
+          // and fetches its part of tile i + 4 between the MFMAs of its stream,
+          // where its VALU and LDS ports are otherwise idle
+          auto stage_hook = [&](auto jc) INLINE {
+            constexpr int j = decltype(jc)::value;
+            constexpr int K0 = 2, V0 = K0 + 2 * KC_PER_T, L0 = V0 + 2 * VU_PER_T;
+            if constexpr (j >= K0 && j < V0 && (j - K0) % 2 == 0) store_k(dst, sg, (j - K0) / 2);
+            if constexpr (j >= V0 && j < L0 && (j - V0) % 2 == 0) store_v(dst, sg, (j - V0) / 2);
+            if constexpr (j == L0) load_tile(kt_load, sg);
+          };
+          // phase Y_i: A streams PV(i), QK(i+1); B takes the softmax of tile i
+          if (A) stream(YES, YES, slot, slot1, stage_hook);
+          else softmax(kt[0]);
+          __syncthreads();
+          // phase X_i+1: B streams PV(i), QK(i+1); A the softmax of tile i+1
+          if (!A) stream(YES, YES, slot, slot1, stage_hook);
+          else if (it + 1 < n_tiles) softmax(kt[1]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
-        kt[4] = tile_or_none(it + 5);
-        __syncthreads();
-        // phase X_i+1
-        if (!grp_a) stream(YES, YES, slot, slot1);
-        else if (it + 1 < n_tiles) softmax(kt[0]);
-        slot = slot1;
-        __syncthreads();
+          for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
+          kt[4] = tile_or_none(it + 5);
+          slot = slot1;
+          __syncthreads();
+        };
+        for (; it + 1 < n_tiles; it += 2) {
+          iteration(sg0);
+          ++it;
+          iteration(sg1);
+          --it;
+        }
+        if (it < n_tiles) iteration(sg0);
       };
-      for (; it + 1 < n_tiles; it += 2) {
-        iteration(sg0);
-        ++it;
-        iteration(sg1);
-        --it;
-      }
-      if (it < n_tiles) iteration(sg0);
+      // group A = waves 0-3, B = waves 4-7 (one wave of each per SIMD)
+      if (__builtin_amdgcn_readfirstlane(wave) < 4) run(YES);
+      else run(NO);
     }
   } else {
     // Two LDS stages, every wave in the same phase: the next list entry's
@@ -600,9 +624,9 @@ prefill_kernel(PrefillArgs a) {
         kt = kt_next;
         if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
       }
-      stream(NO, YES, 0, it & 1);
+      stream(NO, YES, 0, it & 1, no_hook);
       softmax(kt_cur);
-      stream(YES, NO, it & 1, 0);
+      stream(YES, NO, it & 1, 0, no_hook);
       if (more) store_tile(stage((it + 1) & 1), sg);
       __syncthreads();
     }
