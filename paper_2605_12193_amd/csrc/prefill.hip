@@ -306,7 +306,10 @@ prefill_kernel(PrefillArgs a) {
     return (uint32_t)page * page_bytes + (uint32_t)(((key & (ps - 1)) * st + 8 * ce) * 2);
   };
 
-  auto load_tile = [&](int kt, Staged& sg) INLINE {
+  // Fetch this thread's K chunks (part & 1) and/or V units (part & 2) of
+  // tile kt into sg.
+  auto load_part = [&](int kt, Staged& sg, auto part) INLINE {
+    constexpr bool LK = (decltype(part)::value & 1) != 0, LV = (decltype(part)::value & 2) != 0;
     // tiles outside [0, T_kv) (malformed lists) load nothing
     const bool ok = (unsigned)kt < (unsigned)t_kv;
     if (!PAGED) {
@@ -314,11 +317,11 @@ prefill_kernel(PrefillArgs a) {
       const uint32_t base = ok ? (uint32_t)kt * tile_bytes : 0x80000000u;
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
-        if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+        if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
           sg.k[i] = bload16(krs, base + k_boff[i]);
 #pragma unroll
       for (int i = 0; i < VU_PER_T; ++i)
-        if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+        if (LV && (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS)) {
           sg.v[i][0] = bload16(vrs, base + v_boff[i]);
           sg.v[i][1] = bload16(vrs, base + v_boff[i] + st_bytes);
         }
@@ -336,15 +339,19 @@ prefill_kernel(PrefillArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
-      if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+      if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
         sg.k[i] = bload16(krs, paged_off(tok0, k_row[i], k_ce[i], pg));
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
-      if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+      if (LV && (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS)) {
         sg.v[i][0] = bload16(vrs, paged_off(tok0, 2 * v_j[i], v_ce[i], pg));
         sg.v[i][1] = bload16(vrs, paged_off(tok0, 2 * v_j[i] + 1, v_ce[i], pg));
       }
   };
+  const std::integral_constant<int, 1> K_PART;
+  const std::integral_constant<int, 2> V_PART;
+  const std::integral_constant<int, 3> KV_PARTS;
+  auto load_tile = [&](int kt, Staged& sg) INLINE { load_part(kt, sg, KV_PARTS); };
 
   // The staging stores of one thread, as pieces that can be placed apart:
   // K chunk i, and V unit i (two keys x 8 channels, transposed on the way).
@@ -569,23 +576,36 @@ prefill_kernel(PrefillArgs a) {
           const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
           bf16_t* const dst = stage(slot2);
           const int kt_load = kt[4];
-          // the group stages its own part of tile i + 2 (into the free stage)
-          // and fetches its part of tile i + 4 between the MFMAs of its stream,
-          // where its VALU and LDS ports are otherwise idle
+          // The group stages its own part of tile i + 2 (into the stage no one
+          // reads in either phase) and fetches its part of tile i + 4: the K
+          // chunks between the MFMAs of its stream, where its LDS and memory
+          // ports are otherwise idle, and the V units (transposed on the way,
+          // VALU work) in its softmax phase, which is the shorter one.
           auto stage_hook = [&](auto jc) INLINE {
             constexpr int j = decltype(jc)::value;
-            constexpr int K0 = 2, V0 = K0 + 2 * KC_PER_T, L0 = V0 + 2 * VU_PER_T;
-            if constexpr (j >= K0 && j < V0 && (j - K0) % 2 == 0) store_k(dst, sg, (j - K0) / 2);
-            if constexpr (j >= V0 && j < L0 && (j - V0) % 2 == 0) store_v(dst, sg, (j - V0) / 2);
-            if constexpr (j == L0) load_tile(kt_load, sg);
+            constexpr int K0 = 2, L0 = K0 + 2 * KC_PER_T;
+            if constexpr (j >= K0 && j < L0 && (j - K0) % 2 == 0) store_k(dst, sg, (j - K0) / 2);
+            if constexpr (j == L0) load_part(kt_load, sg, K_PART);
+          };
+          auto softmax_v = [&](int kt_s) INLINE {
+#pragma unroll
+            for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
+            load_part(kt_load, sg, V_PART);
+            softmax(kt_s);
           };
           // phase Y_i: A streams PV(i), QK(i+1); B takes the softmax of tile i
           if (A) stream(YES, YES, slot, slot1, stage_hook);
-          else softmax(kt[0]);
+          else softmax_v(kt[0]);
           __syncthreads();
           // phase X_i+1: B streams PV(i), QK(i+1); A the softmax of tile i+1
-          if (!A) stream(YES, YES, slot, slot1, stage_hook);
-          else if (it + 1 < n_tiles) softmax(kt[1]);
+          if (!A) {
+            stream(YES, YES, slot, slot1, stage_hook);
+          } else {
+#pragma unroll
+            for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
+            load_part(kt_load, sg, V_PART);
+            if (it + 1 < n_tiles) softmax(kt[1]);
+          }
 #pragma unroll
           for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
           kt[4] = tile_or_none(it + 5);
