@@ -278,9 +278,11 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = start.elapsed_time(end) / args.steps
-    st1 = float(np.mean([m[0].elapsed_time(m[1]) for m in marks]))
-    exp_ms = float(np.mean([m[1].elapsed_time(m[2]) for m in marks]))
-    pre_ms = float(np.mean([m[2].elapsed_time(m[3]) for m in marks]))
+    per_step = {name: [m[i].elapsed_time(m[i + 1]) for m in marks]
+                for i, name in enumerate(("estimate_mask", "expand_rescue", "sparse_prefill"))}
+    st1 = float(np.mean(per_step["estimate_mask"]))
+    exp_ms = float(np.mean(per_step["expand_rescue"]))
+    pre_ms = float(np.mean(per_step["sparse_prefill"]))
     log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
 
     # dense baseline (same kernel family, every causal tile)
@@ -340,6 +342,8 @@ def main():
         "config": config,
         "stage_ms": {"estimate_mask": round(st1, 3), "expand_rescue": round(exp_ms, 3),
                      "sparse_prefill": round(pre_ms, 3)},
+        "stage_ms_min_median_max": {k: [round(float(np.min(v)), 3), round(float(np.median(v)), 3),
+                                        round(float(np.max(v)), 3)] for k, v in per_step.items()},
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(flop_dense / (dense_ms * 1e-3) / 1e12, 2),
         "speedup_vs_dense": round(dense_ms / ms_step, 3),

@@ -1,0 +1,64 @@
+"""Every (head dim, GQA group) shape the prefill kernels instantiate, against
+the oracle: C in {64, 128, 256} x m in {1, 2, 4, 5, 8}.  Each runs a ragged
+333-token request (five full tiles and a 13-token tail) through the sparse
+prefill on the oracle's own lists and through the dense prefill.  This covers
+the ping-pong shapes (m = 4, 8 at C <= 128), the two-stage shapes and the
+half-tile shapes, including those whose registers spill (C = 256 with
+m in {1, 5, 8})."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bfla_oracle as O
+from paper_2605_12193_amd import bfla, synth
+from parity_util import DeviceBatch, compare_outputs, lists_to_device, oracle_lists_for
+
+pytestmark = pytest.mark.gpu
+
+N = 333
+CASES = [(c, m) for c in (64, 128, 256) for m in (1, 2, 4, 5, 8)]
+IDS = [f"c{c}_m{m}" for c, m in CASES]
+
+
+def _batch(c, m):
+    wl = synth.workload("tiny_2k", h_q=m, h_kv=1, head_dim=c, seed=100 + c + m)
+    return DeviceBatch(synth.make_inputs(wl, seqlens=[N]), None)
+
+
+def _params():
+    kw = dict(block=128, group=64, tile=64, gamma=0.9, n_local=2, n_sink=1, eta=16,
+              rho=0.1, seed=5)
+    return kw, bfla.params(**kw)
+
+
+def _check_lse(got, want):
+    np.testing.assert_allclose(got.reshape(want.shape), want, rtol=0, atol=2e-4)
+
+
+@pytest.mark.parametrize("c,m", CASES, ids=IDS)
+def test_sparse_shape(c, m):
+    db = _batch(c, m)
+    kw, prm = _params()
+    q, k, v = db.host(0)
+    st = O.estimate_mask(q, k, kw["block"], kw["group"], kw["gamma"], O.default_scale(c))
+    rp, cols, _ = oracle_lists_for(db, [st["mask"]], kw)
+    drp, dcols = lists_to_device(rp, cols)
+    lse = torch.full((m * N,), float("nan"), device="cuda")
+    bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, drp, dcols, db.ov, lse)
+    torch.cuda.synchronize()
+    want, want_lse = O.attention(q, k, v, 64, O.default_scale(c), rp, cols, 0)
+    compare_outputs(db.o_of(0), want, f"sparse C={c} m={m}")
+    _check_lse(lse.cpu().numpy(), want_lse)
+
+
+@pytest.mark.parametrize("c,m", CASES, ids=IDS)
+def test_dense_shape(c, m):
+    db = _batch(c, m)
+    _, prm = _params()
+    lse = torch.full((m * N,), float("nan"), device="cuda")
+    bfla.bfla_dense_prefill(db.prob, prm, db.qv, db.kv, db.ov, lse)
+    torch.cuda.synchronize()
+    q, k, v = db.host(0)
+    want, want_lse = O.attention(q, k, v, 64, O.default_scale(c))
+    compare_outputs(db.o_of(0), want, f"dense C={c} m={m}")
+    _check_lse(lse.cpu().numpy(), want_lse)
