@@ -368,12 +368,35 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
   if (a.gamma >= 1.0f) {
     for (int j = tid; j < n_causal; j += blockDim.x) atomicOr(&keep_bits[j >> 5], 1u << (j & 31));
   } else {
+    // Rows of up to 64 * ROW_REGS causal blocks (every row up to 128K tokens
+    // at b = 128) are read once into registers, lane l holding blocks
+    // l, l + 64, ...; longer rows are re-read from memory on every pass.  Both
+    // paths visit the blocks in the same per-lane order, so the statistics and
+    // the picks are bit-identical.
+    constexpr int ROW_REGS = 16;
+    const bool in_regs = n_causal <= 64 * ROW_REGS;
+    float rv[ROW_REGS];
+#pragma unroll
+    for (int k = 0; k < ROW_REGS; ++k) {
+      const int j = lane + 64 * k;
+      rv[k] = (in_regs && j < n_causal) ? row[j] : -INFINITY;
+    }
+    // f(j, s) for every causal block j of this lane, in increasing j
+    auto for_each = [&](auto&& f) __attribute__((always_inline)) {
+      if (in_regs) {
+#pragma unroll
+        for (int k = 0; k < ROW_REGS; ++k)
+          if (lane + 64 * k < n_causal) f(lane + 64 * k, rv[k]);
+      } else {
+        for (int j = lane; j < n_causal; j += 64) f(j, row[j]);
+      }
+    };
     // softmax statistics (eq15)
     float mx = -INFINITY;
-    for (int j = lane; j < n_causal; j += 64) mx = fmaxf(mx, row[j]);
+    for_each([&](int, float s) { mx = fmaxf(mx, s); });
     for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
     float z = 0.f;
-    for (int j = lane; j < n_causal; j += 64) z += expf(a.alpha * (row[j] - mx));
+    for_each([&](int, float s) { z += expf(a.alpha * (s - mx)); });
     for (int d = 32; d >= 1; d >>= 1) z += __shfl_xor(z, d);
 
     // keep-mass selection (eq16-eq18): repeated arg-max below the last pick
@@ -383,10 +406,9 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
     for (int taken = 0; taken < n_causal; ++taken) {
       float bs = -INFINITY;
       int bj = INT_MAX;
-      for (int j = lane; j < n_causal; j += 64) {
-        const float s = row[j];
+      for_each([&](int j, float s) {
         if (better(s_prev, j_prev, s, j) && better(s, j, bs, bj)) { bs = s; bj = j; }
-      }
+      });
       for (int d = 32; d >= 1; d >>= 1) {
         const float os = __shfl_xor(bs, d);
         const int oj = __shfl_xor(bj, d);
