@@ -399,6 +399,13 @@ prefill_kernel(PrefillArgs a) {
     return DENSE ? i : uniform_load(a.cols, __builtin_amdgcn_readfirstlane(list_begin + i));
   };
   auto stage = [&](int slot) INLINE -> bf16_t* { return lds + slot * CF::STAGE; };
+  // List entry i, or -1 (a tile that loads zeros) past the end.  The list
+  // read itself is unconditional (index clamped) so that it stays a scalar
+  // load: a vector load would share vmcnt with the K/V prefetch.
+  auto tile_or_none = [&](int i) INLINE -> int {
+    const int t = tile_at(min(i, n_tiles - 1));
+    return i < n_tiles ? t : -1;
+  };
 
   // ---- MFMA streams fed from LDS ----
   // S^T = K . Q^T (two 32-key blocks, Q held in registers) and
@@ -539,12 +546,6 @@ prefill_kernel(PrefillArgs a) {
     // Past the end of the list the loads read zeros (no memory traffic) and
     // the stores fill a stage no one reads, so the loop body has no branches
     // around its memory operations.
-    // the list read itself is unconditional (index clamped) so that it stays
-    // a scalar load: a vector load would share vmcnt with the K/V prefetch
-    auto tile_or_none = [&](int i) INLINE -> int {
-      const int t = tile_at(min(i, n_tiles - 1));
-      return i < n_tiles ? t : -1;
-    };
     if (n_tiles > 0) {
       Staged sg0, sg1;
       int kt[5];  // tiles i .. i+4
@@ -625,30 +626,35 @@ prefill_kernel(PrefillArgs a) {
       else run(NO);
     }
   } else {
-    // Two LDS stages, every wave in the same phase: the next list entry's
-    // tile is fetched into registers while the current one is consumed.
-    Staged sg;
-    int kt_next = 0;
+    // Two LDS stages, every wave in the same phase.  Tile i + 1 (fetched into
+    // registers during iteration i - 1) is stored into the free stage, and
+    // tile i + 2 fetched, between the MFMAs of the PV stream of iteration i,
+    // where the wave's VALU and LDS ports are otherwise idle.  Past the end of
+    // the list the loads read zeros and the stores fill the unused stage.
     if (n_tiles > 0) {
+      Staged sg;
       load_tile(tile_at(0), sg);
       store_tile(stage(0), sg);
-      if (n_tiles > 1) kt_next = tile_at(1);
-    }
-    __syncthreads();
-    int kt = n_tiles > 0 ? tile_at(0) : 0;
-    for (int it = 0; it < n_tiles; ++it) {
-      const bool more = it + 1 < n_tiles;
-      const int kt_cur = kt;
-      if (more) {
-        load_tile(kt_next, sg);
-        kt = kt_next;
-        if (it + 2 < n_tiles) kt_next = tile_at(it + 2);
-      }
-      stream(NO, YES, 0, it & 1, no_hook);
-      softmax(kt_cur);
-      stream(YES, NO, it & 1, 0, no_hook);
-      if (more) store_tile(stage((it + 1) & 1), sg);
+      load_tile(tile_or_none(1), sg);
       __syncthreads();
+      int kt_cur = tile_at(0);
+      for (int it = 0; it < n_tiles; ++it) {
+        bf16_t* const dst = stage((it + 1) & 1);
+        const int kt_load = tile_or_none(it + 2);
+        auto stage_hook = [&](auto jc) INLINE {
+          constexpr int j = decltype(jc)::value;
+          constexpr int K0 = 1, V0 = K0 + KC_PER_T, L0 = V0 + VU_PER_T;
+          static_assert(L0 < 4 * NCB, "staging pieces must fit the PV stream");
+          if constexpr (j >= K0 && j < V0) store_k(dst, sg, j - K0);
+          if constexpr (j >= V0 && j < L0) store_v(dst, sg, j - V0);
+          if constexpr (j == L0) load_tile(kt_load, sg);
+        };
+        stream(NO, YES, 0, it & 1, no_hook);
+        softmax(kt_cur);
+        stream(YES, NO, it & 1, 0, stage_hook);
+        kt_cur = tile_or_none(it + 1);
+        __syncthreads();
+      }
     }
   }
 
