@@ -54,15 +54,15 @@ extern "C" {
 typedef enum bfla_status {
   BFLA_OK = 0,
   BFLA_ERR_INVALID_ARG = 1,  /* null pointer, bad size, out-of-range value */
-  BFLA_ERR_UNSUPPORTED = 2,  /* valid but not built: head_dim, tile, block */
+  BFLA_ERR_UNSUPPORTED = 2,  /* valid but not built: head_dim, tile, block, m */
   BFLA_ERR_WORKSPACE = 3,    /* workspace smaller than bfla_workspace_size */
   BFLA_ERR_CAPACITY = 4,     /* cols capacity below bfla_list_capacity */
   BFLA_ERR_HIP = 5           /* a HIP launch failed; see bfla_last_error */
 } bfla_status;
 
 /* Problem statement (eq2-eq3): head-first Q [H_q][N_q][C] and K/V
- * [H_kv][N_kv][C] per request, GQA group size m = H_q / H_kv; query head p
- * reads KV head floor(p / m) (eq8).  Request r has N_q = n_q[r] query tokens
+ * [H_kv][N_kv][C] per request, GQA group size m = H_q / H_kv (1 to 8 are
+ * built); query head p reads KV head floor(p / m) (eq8).  Request r has N_q = n_q[r] query tokens
  * that are the LAST N_q of its N_kv = n_kv[r] tokens (chunked prefill with a
  * prefix of N_c = N_kv - N_q tokens, eq11). */
 typedef struct bfla_problem {
@@ -173,8 +173,8 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
  *   block_mask  out, device uint8, layout above.
  *   dbg_scores  out, device float or NULL.
  *   workspace   device scratch of >= bfla_workspace_size(BFLA_WS_ESTIMATE).
- * Errors: INVALID_ARG, UNSUPPORTED (also: more than 65536 KV blocks per
- * request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
+ * Errors: INVALID_ARG, UNSUPPORTED (also: m > 8; more than 65536 KV blocks
+ * per request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
  * i.e. (128 g - 1) * stride_tok + head_dim >= 2^30; paged K where 128 g
  * tokens may span more than 2048 pages), WORKSPACE, HIP. */
 int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params,

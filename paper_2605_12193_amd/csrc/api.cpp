@@ -259,7 +259,7 @@ int prefill_common(const bfla_problem* prob, const bfla_params* pr, const bfla_v
   if ((st = check_kv(prob, kv, true))) return st;
   if ((st = check_rows_fit(sizes_of(prob, pr)))) return st;
   if (!prefill_supported(prob->head_dim, prob->h_q / prob->h_kv))
-    return fail(BFLA_ERR_UNSUPPORTED, "GQA group size %d not built (1, 2, 4, 5, 8)",
+    return fail(BFLA_ERR_UNSUPPORTED, "GQA group size %d not built (1 to 8)",
                 prob->h_q / prob->h_kv);
   L->q = q->data;
   L->o = o->data;
@@ -332,6 +332,9 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   if ((st = check_view(prob, q, "q"))) return st;
   if ((st = check_kv(prob, kv, false))) return st;
   if (!block_mask) return fail(BFLA_ERR_INVALID_ARG, "block_mask is NULL");
+  if (prob->h_q / prob->h_kv > 8)
+    return fail(BFLA_ERR_UNSUPPORTED, "GQA group size %d not built (1 to 8)",
+                prob->h_q / prob->h_kv);
   if (!estimate_supported(prob->head_dim, params->block, params->group))
     return fail(BFLA_ERR_UNSUPPORTED, "block %d / group %d not built for head_dim %d",
                 params->block, params->group, prob->head_dim);

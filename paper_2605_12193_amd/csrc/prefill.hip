@@ -171,12 +171,13 @@ __device__ __forceinline__ void lgkm_wait(u32x4& r) {
 
 // Shapes whose 2m-wave workgroup would cap registers below what the loop
 // needs run half q-tiles instead: m waves of 32 queries, one per head, still
-// sharing every K/V tile across the group.  That is m = 5 (3 waves on a SIMD)
-// and m = 8 (16 waves), and m = 4 at C = 256 (two waves per SIMD cannot hold
-// the 256-channel accumulators).
+// sharing every K/V tile across the group.  At C <= 128 that is m > 4 (more
+// than two waves on a SIMD); at C = 256, m > 2 (two waves per SIMD cannot
+// hold the 256-channel accumulators).
+__host__ __device__ constexpr bool half_shape(int c, int m) { return c == 256 ? m > 2 : m > 4; }
 template <int C, int M>
 struct Shape {
-  static constexpr bool HALF = (M == 5 || M == 8 || (C == 256 && M == 4));
+  static constexpr bool HALF = half_shape(C, M);
   static constexpr int WAVES = HALF ? M : 2 * M;
 };
 
@@ -709,7 +710,10 @@ hipError_t launch_c(const PrefillArgs& a, bool dense, int n_work, hipStream_t s)
     case 1: return launch_c_m<C, 1>(a, dense, n_work, s);
     case 2: return launch_c_m<C, 2>(a, dense, n_work, s);
     case 4: return launch_c_m<C, 4>(a, dense, n_work, s);
+    case 3: return launch_c_m<C, 3>(a, dense, n_work, s);
     case 5: return launch_c_m<C, 5>(a, dense, n_work, s);
+    case 6: return launch_c_m<C, 6>(a, dense, n_work, s);
+    case 7: return launch_c_m<C, 7>(a, dense, n_work, s);
     case 8: return launch_c_m<C, 8>(a, dense, n_work, s);
     default: return hipErrorInvalidValue;
   }
@@ -719,7 +723,7 @@ hipError_t launch_c(const PrefillArgs& a, bool dense, int n_work, hipStream_t s)
 
 bool prefill_supported(int head_dim, int m) {
   bool c_ok = head_dim == 64 || head_dim == 128 || head_dim == 256;
-  bool m_ok = m == 1 || m == 2 || m == 4 || m == 5 || m == 8;
+  bool m_ok = m >= 1 && m <= 8;
   return c_ok && m_ok;
 }
 
@@ -741,7 +745,7 @@ hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
   a.scale = L.scale;
   a.batch = L.batch;
   // work items per (request, KV head, q-tile): two for the half-tile shapes
-  const bool half = a.m == 5 || a.m == 8 || (L.head_dim == 256 && a.m == 4);
+  const bool half = half_shape(L.head_dim, a.m);
   const int per_row = half ? 2 : 1;
   int n_work = 0;
   for (int i = 0; i < a.batch.n_req; ++i) {

@@ -129,8 +129,8 @@ def test_entry_points_reject_before_launch():
     st = L.bfla_sparse_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), None,
                                None, C.byref(v), None, None)
     assert st == bfla.BFLA_ERR_INVALID_ARG
-    # unsupported GQA group size 3
-    p3 = bfla.Problem([256], [256], 6, 2, 64)
+    # unsupported GQA group size 9
+    p3 = bfla.Problem([256], [256], 18, 2, 64)
     st = L.bfla_dense_prefill(C.byref(p3.c), C.byref(prm), C.byref(v), C.byref(kv),
                               C.byref(v), None, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
