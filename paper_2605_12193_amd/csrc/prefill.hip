@@ -4,8 +4,8 @@
 // Work item = one list row (request r, KV head h, query tile qt): all m
 // query heads of the GQA group share every K/V tile load.  Each wave owns 32
 // queries of one head: 2 waves per head (2m per workgroup), or, for the
-// half-tile shapes (m = 5, 8; m = 4 at C = 256), one wave per head over half
-// the q-tile, two work items per row.
+// half-tile shapes (m > 4 at C <= 128, m > 2 at C = 256), one wave per head
+// over half the q-tile, two work items per row.
 //
 // Per KV tile (T = 64 keys):
 //   S^T[key][query] = K_tile . Q^T   v_mfma_f32_32x32x16_bf16, K from LDS
@@ -18,11 +18,12 @@
 //   V is staged transposed in LDS with the key order inside every 16-key
 //   chunk permuted (bits 2 and 3 of the key offset swapped) so that the
 //   accumulator's key order and the A operand's agree.
-// K/V tiles are fetched into registers one list entry ahead and stored into
-// LDS stages (two, or three in the ping-pong schedule of the 8-wave shapes)
-// while earlier tiles are consumed.  K/V are read through buffer descriptors
-// whose range check returns zeros past the last key or page, so loads carry
-// no branches.
+// K/V tiles go from memory into registers and from there into LDS stages
+// (three in the ping-pong schedule of the 8-wave shapes, two otherwise), the
+// staging instructions placed between the MFMAs of a stream: two iterations
+// ahead through two register sets in the ping-pong, one ahead otherwise.
+// K/V are read through buffer descriptors whose range check returns zeros
+// past the last key or page, so loads carry no branches.
 //
 // The lane ^ 32 exchanges of the row max and sum use v_permlane32_swap.
 //
