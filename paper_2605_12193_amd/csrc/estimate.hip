@@ -6,7 +6,7 @@
 // is a GEMM whose rows are flattened g-token query groups and whose columns
 // are flattened key groups (inner dimension g*C; a flattened group of a
 // row-major [N][C] head is g consecutive token rows, so no copy is made,
-// eq6-eq7).  256 x 128 output tiles, 4 waves of 64 x 128, bf16 MFMA
+// eq6-eq7).  256 x 128 output tiles, 8 waves of 32 x 128, bf16 MFMA
 // 32x32x16; Q/K chunks of 64 inner elements go from buffer loads straight
 // into a 3-slot LDS ring (two chunks in flight, one workgroup per CU);
 // only tiles holding a causal block pair are computed (eq11-eq14).  The
@@ -26,10 +26,15 @@
 namespace bfla {
 namespace {
 
-constexpr int BM = 256;     // query groups per tile (64 per wave)
+constexpr int BM = 256;     // query groups per tile (32 per wave)
 constexpr int BN = 128;     // key groups per tile
 constexpr int BK = 64;      // inner elements per stage
-constexpr int NT = 256;
+// 8 waves (two per SIMD): each keeps its own DMA loads in flight, and the
+// kernel is bound by the memory requests in flight (4 waves of 64 x 128
+// outputs each were 12 % slower)
+constexpr int NW = 8;
+constexpr int NT = 64 * NW;
+constexpr int XB = BM / NW / 32;   // 32-row MFMA blocks per wave
 constexpr int CHAIN = 8;    // stages per inner accumulation chain (32 MFMA k-steps)
 constexpr int MAX_LKV = 65536;
 
@@ -71,8 +76,8 @@ __host__ __device__ __forceinline__ int col_tiles(int groups) { return (groups +
 constexpr int A_ELEMS = BM * BK;
 constexpr int B_ELEMS = BN * BK;
 constexpr int NSTAGE = 3;     // ring depth: loads run NSTAGE - 1 stages ahead
-constexpr int A_LOADS = BM / 8 / 4;   // 1 KB loads per wave per stage (8 rows each)
-constexpr int B_LOADS = BN / 8 / 4;
+constexpr int A_LOADS = BM / 8 / NW;   // 1 KB loads per wave per stage (8 rows each)
+constexpr int B_LOADS = BN / 8 / NW;
 constexpr int VM_STAGE = A_LOADS + B_LOADS;
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;
 constexpr int PT_MAX = 2048;  // page-table entries one tile of a paged cache may span
@@ -145,8 +150,8 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   }
 
   // ---- direct global -> LDS loads through buffer descriptors ----
-  // Wave w, load i fills rows [8 (4 i + w), +8) of the Q (i < A_LOADS) or K
-  // (i < B_LOADS) tile: lane l writes LDS chunk l % 8 of row 8 (4 i + w) +
+  // Wave w, load i fills rows [8 (NW i + w), +8) of the Q (i < A_LOADS) or K
+  // (i < B_LOADS) tile: lane l writes LDS chunk l % 8 of row 8 (NW i + w) +
   // l / 8 and fetches the logical chunk that the swizzle places there.  Out-of-range offsets
   // (padding groups, tokens past the end, bad pages) read as zeros.  The Q
   // descriptor starts at the tile's first query token, so it spans at most
@@ -181,7 +186,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   bool q_ok[A_LOADS], k_ok[B_LOADS];
 #pragma unroll
   for (int i = 0; i < A_LOADS; ++i) {
-    const int row = 8 * (4 * i + wave) + row_sub;   // the K rows are the first B_LOADS of these
+    const int row = 8 * (NW * i + wave) + row_sub;   // the K rows are the first B_LOADS of these
     lch[i] = swz(row, pch);
     q_ok[i] = ti * BM + row < nqg;
     q_row_tok[i] = row * a.g;   // relative to q_tok0
@@ -204,7 +209,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
       const uint32_t qo = (q_ok[i] && tq < q_tile_tok)
                               ? (uint32_t)(((int64_t)tq * a.q_st + ch + 8 * lch[i]) * 2)
                               : 0x80000000u;
-      dma16(qrs, la + i * 4096, qo);
+      dma16(qrs, la + i * (NW * 1024), qo);
     }
 #pragma unroll
     for (int i = 0; i < B_LOADS; ++i) {
@@ -220,14 +225,14 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
           ko = (uint32_t)(((int64_t)tk * a.kv.stride_tok + ch + 8 * lch[i]) * 2);
         }
       }
-      dma16(krs, lb + i * 4096, ko);
+      dma16(krs, lb + i * (NW * 1024), ko);
     }
   };
 
-  // wave w: query-group rows [64 w, +64) x all BN key-group columns
-  f32x16 acc[2][4], tot[2][4];
+  // wave w: query-group rows [32 w, +32) x all BN key-group columns
+  f32x16 acc[XB][4], tot[XB][4];
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
+  for (int x = 0; x < XB; ++x)
 #pragma unroll
     for (int y = 0; y < 4; ++y)
 #pragma unroll
@@ -237,10 +242,10 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   auto compute = [&](const bf16_t* A, const bf16_t* B) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[2], bf[4];
+      bf16x8 af[XB], bf[4];
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        const int row = 64 * wave + 32 * x + l32;
+      for (int x = 0; x < XB; ++x) {
+        const int row = (BM / NW) * wave + 32 * x + l32;
         af[x] = __builtin_bit_cast(bf16x8, ld16(A + row * BK + 8 * swz(row, 2 * ks + hi)));
       }
 #pragma unroll
@@ -249,7 +254,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
         bf[y] = __builtin_bit_cast(bf16x8, ld16(B + row * BK + 8 * swz(row, 2 * ks + hi)));
       }
 #pragma unroll
-      for (int x = 0; x < 2; ++x)
+      for (int x = 0; x < XB; ++x)
 #pragma unroll
         for (int y = 0; y < 4; ++y) acc[x][y] = mfma32(af[x], bf[y], acc[x][y]);
     }
@@ -278,7 +283,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
     }
     // close the chain: fold it into the running total
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < XB; ++x)
 #pragma unroll
       for (int y = 0; y < 4; ++y)
 #pragma unroll
@@ -289,14 +294,14 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   // D[row = query group][col = key group]; lane: col l32, rows 8(r/4)+4hi+r%4
   float* srow_base = a.scores + R.score_off + (int64_t)p * R.l_q * R.l_kv;
 #pragma unroll
-  for (int x = 0; x < 2; ++x) {
+  for (int x = 0; x < XB; ++x) {
 #pragma unroll
     for (int y = 0; y < 4; ++y) {
       const int gj = tj * BN + 32 * y + l32;
       f32x16 v = tot[x][y];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int gi = ti * BM + 64 * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
+        const int gi = ti * BM + (BM / NW) * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
         if (gi >= nqg || gj >= nkg) v[r] = -INFINITY;
       }
       // pool over G consecutive query-group rows
@@ -332,7 +337,7 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
       if (j >= R.l_kv) continue;
 #pragma unroll
       for (int r = 0; r < 16; r += (G >= 16 ? 8 : G >= 4 ? 4 : G)) {
-        const int gi = ti * BM + 64 * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
+        const int gi = ti * BM + (BM / NW) * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
         const int i = gi / G;
         if (i >= R.l_q) continue;
         const int e_i = min(n_c + (i + 1) * a.b - 1, R.n_kv - 1);
