@@ -1,0 +1,58 @@
+"""Host-side logic of bench.py (no GPU): the dense-equivalent FLOP count, the
+committed traffic profiles it reads, and the one-GPU guard."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_dense_equiv_flop_closed_form():
+    # full prefill: query t attends t + 1 keys -> 4 C H_q N (N + 1) / 2
+    n, h_q, c = 1000, 3, 64
+    assert bench.dense_equiv_flop([n], [n], h_q, c) == 4.0 * c * h_q * n * (n + 1) / 2
+    # chunked: the last n_q of n_kv tokens, query t attends n_c + t + 1 keys
+    n_kv, n_q = 900, 100
+    want = 4.0 * c * h_q * sum(n_kv - n_q + t + 1 for t in range(n_q))
+    assert bench.dense_equiv_flop([n_kv], [n_q], h_q, c) == want
+    # a batch is the sum of its requests
+    assert bench.dense_equiv_flop([n, n_kv], [n, n_q], h_q, c) == pytest.approx(
+        bench.dense_equiv_flop([n], [n], h_q, c) + want)
+
+
+def test_committed_traffic_profiles_match_the_kernel_source():
+    # every committed prefill traffic summary names the current source hash, so
+    # the bench line reports measured HBM bytes for the kernel it times
+    for wl in ("llama_128k", "llama_32k", "wide_64k", "paged_4x"):
+        path = os.path.join(ROOT, "profiles", "prefill_" + wl.replace("_", "") + "_traffic.md")
+        if not os.path.exists(path):
+            continue
+        traffic = bench.measured_traffic(wl)
+        assert traffic is not None and traffic > 0, f"{wl}: stale or unreadable traffic profile"
+    assert bench.measured_traffic("no_such_workload") is None
+
+
+def test_source_hash_ignores_comments(tmp_path, monkeypatch):
+    src = tmp_path / "paper_2605_12193_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "bfla_device.h").write_text("int x;\n")
+    (src / "prefill.hip").write_text("int f() { return 1; }  // one\n/* block */\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    h1 = bench.prefill_source_hash()
+    (src / "prefill.hip").write_text("// header\nint f() {\n  return 1;\n}\n")
+    assert bench.prefill_source_hash() == h1
+    (src / "prefill.hip").write_text("int f() { return 2; }\n")
+    assert bench.prefill_source_hash() != h1
+
+
+def test_more_than_one_gpu_is_refused():
+    out = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert out.returncode == 2
+    msg = json.loads(out.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
