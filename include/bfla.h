@@ -33,6 +33,10 @@
  *    been enqueued and the outputs are untouched.
  *  - Outputs are fully overwritten and bit-identical across runs (no
  *    floating-point atomics).
+ *  - Calls only launch kernels (no allocation, memset, copy or
+ *    synchronisation), so they can be captured into a HIP graph; run each
+ *    kernel shape once outside capture first (its first launch sets the
+ *    kernel's dynamic-LDS attribute).
  *  - No C++ exception crosses the ABI.  There is no global mutable state;
  *    the last error message is thread-local.
  */
