@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "sparse prefill ms + dense-equiv TFLOP/s at 32K/128K; speedup vs dense; rel-err"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
 def log(msg):
@@ -61,12 +62,16 @@ def parse():
     return ap.parse_args()
 
 
-def prefill_source_hash() -> str:
-    """Hash of the prefill kernel's code (prefill.hip and the device header)
+PREFILL_SOURCES = ("paper_2605_12193_amd/csrc/prefill.hip", "paper_2605_12193_amd/csrc/bfla_device.h")
+SCORES_SOURCES = ("paper_2605_12193_amd/csrc/estimate.hip", "paper_2605_12193_amd/csrc/bfla_device.h")
+
+
+def prefill_source_hash(files=PREFILL_SOURCES) -> str:
+    """Hash of a kernel's code (by default prefill.hip and the device header)
     with comments and whitespace removed, so only code changes invalidate a
     committed traffic profile."""
     m = hashlib.sha256()
-    for f in ("paper_2605_12193_amd/csrc/prefill.hip", "paper_2605_12193_amd/csrc/bfla_device.h"):
+    for f in files:
         with open(os.path.join(ROOT, f)) as fh:
             text = fh.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
@@ -75,10 +80,11 @@ def prefill_source_hash() -> str:
     return m.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per sparse-prefill launch from the committed rocprofv3 counter
-    summary, or None if there is none for this workload or the kernel source
-    changed since the counters were taken."""
+def measured_traffic(workload: str, key: str = "traffic_bytes_prefill_sparse"):
+    """HBM bytes per launch of a kernel (the sparse prefill by default, or
+    key="traffic_bytes_scores" for the Stage-1 score kernel) from the
+    committed rocprofv3 counter summary, or None if there is none for this
+    workload or that kernel's source changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "prefill_" + workload.replace("_", "") + "_traffic.md")
     if not os.path.exists(path):
         return None
@@ -87,9 +93,14 @@ def measured_traffic(workload: str):
         parts = line.split()
         if len(parts) == 2:
             kv[parts[0]] = parts[1]
-    if kv.get("source_hash") != prefill_source_hash() or kv.get("workload") != workload:
+    if kv.get("workload") != workload:
         return None
-    v = kv.get("traffic_bytes_prefill_sparse")
+    if key == "traffic_bytes_scores":
+        if kv.get("scores_source_hash") != prefill_source_hash(SCORES_SOURCES):
+            return None
+    elif kv.get("source_hash") != prefill_source_hash():
+        return None
+    v = kv.get(key)
     return float(v) if v else None
 
 
@@ -100,6 +111,22 @@ def dense_equiv_flop(n_kv, n_q, h_q, c):
     for nk, nq in zip(n_kv, n_q):
         tot += nq * (nk - nq) + nq * (nq + 1) // 2
     return 4.0 * c * h_q * tot
+
+
+def stage1_work(n_kv, n_q, h_q, h_kv, c, b, g):
+    """Algorithmic work of the Stage-1 score GEMM: 2 g C FLOP for each of the
+    G^2 group pairs (G = b / g) of every causal (query block, KV block) pair
+    of every query head (eq9-eq14), and Q and K read once (2 B per element)."""
+    G = b // g
+    pairs = 0
+    for nk, nq in zip(n_kv, n_q):
+        nc = nk - nq
+        for i in range(-(-nq // b)):
+            e = min(nc + (i + 1) * b - 1, nk - 1)
+            pairs += e // b + 1
+    flop = 2.0 * g * c * G * G * h_q * pairs
+    nbytes = 2.0 * c * sum(h_q * nq + h_kv * nk for nk, nq in zip(n_kv, n_q))
+    return flop, nbytes
 
 
 class Inputs:
@@ -142,11 +169,14 @@ class Inputs:
         return o[a + t0:a + t1, p].float().cpu().numpy()
 
 
-def cpu_baseline(wl, inp, gpu_o, budget_s, seed=0):
+def cpu_baseline(wl, inp, gpu_o, budget_s, gpu_mask=None, seed=0):
     """Time the oracle on random (request, KV head, q-tile) rows: Stage 1 of
     the query block holding the q-tile (all m query heads of the KV head), the
     tile stage of that block row, and the sparse attention of the q-tile.
-    Also returns the GPU-vs-oracle error on the sampled outputs."""
+    Also returns the GPU-vs-oracle error on the sampled outputs and, given the
+    GPU block mask (host uint8, the library's packed layout), its agreement
+    with the oracle's mask on the sampled block rows: every sure cell must
+    match; near-tie cells are counted, and so are the ones that differ."""
     from oracle import bfla_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -161,6 +191,10 @@ def cpu_baseline(wl, inp, gpu_o, budget_s, seed=0):
     order = rng.permutation(len(rows))
     heads = rng.integers(0, wl.h_kv, len(rows))
     host = {}
+    L = [-(-n // b) for n in inp.n]
+    mask_off = np.concatenate([[0], np.cumsum([wl.h_kv * x * x for x in L])]).astype(np.int64)
+    mchk = {"block_rows": 0, "blocks": 0, "sure_mismatch": 0, "tie_blocks": 0, "tie_mismatch": 0}
+    seen = set()
     flop = 0.0
     max_abs, num, den = 0.0, 0.0, 0.0
     t0 = time.perf_counter()
@@ -182,6 +216,18 @@ def cpu_baseline(wl, inp, gpu_o, budget_s, seed=0):
                              wl.group, wl.gamma, alpha)
         bm = np.zeros((-(-n // b), -(-n // b)), np.uint8)
         bm[i, :st["mask"].shape[2]] = st["mask"][0, 0]
+        if gpu_mask is not None and (r, h, i) not in seen:
+            seen.add((r, h, i))
+            lr = L[r]
+            row0 = int(mask_off[r]) + (h * lr + i) * lr
+            got = gpu_mask[row0:row0 + st["mask"].shape[2]]
+            want, status = st["mask"][0, 0], st["status"][0, 0]
+            tie = status == O.TIE
+            mchk["block_rows"] += 1
+            mchk["blocks"] += int(want.size)
+            mchk["sure_mismatch"] += int(np.sum((got != want) & ~tie))
+            mchk["tie_blocks"] += int(np.sum(tie))
+            mchk["tie_mismatch"] += int(np.sum((got != want) & tie))
         tm = O.tile_mask(bm, n, n, b, T, wl.n_local, wl.n_sink, wl.eta, wl.rho, wl.seed, h)
         tiles = np.flatnonzero(tm[qt])
         for pp in range(m):
@@ -201,7 +247,7 @@ def cpu_baseline(wl, inp, gpu_o, budget_s, seed=0):
                    f"and the row's sparse attention; {dt:.1f} s; value = dense-equivalent "
                    f"FLOP of the sampled rows / oracle time"),
         "seconds": dt,
-    }, {"max_abs": max_abs, "rel_l2": math.sqrt(num / max(den, 1e-30))}
+    }, {"max_abs": max_abs, "rel_l2": math.sqrt(num / max(den, 1e-30))}, mchk
 
 
 def main():
@@ -320,6 +366,26 @@ def main():
         den += float(torch.sum(b ** 2))
     sd_err = math.sqrt(num / max(den, 1e-30))
 
+    # Stage 1 (estimate_mask: score GEMM + selection) against both rooflines:
+    # algorithmic FLOP over its time vs the MFMA peak, and the score kernel's
+    # measured HBM bytes (committed rocprofv3 counters) over the same time vs
+    # the HBM peak (a lower bound on the kernel's own rate, since the stage
+    # time also holds the selection kernel)
+    f1, b1 = stage1_work(inp.n, inp.n, wl.h_q, wl.h_kv, wl.head_dim, wl.block, wl.group)
+    t1 = measured_traffic(wl.name, "traffic_bytes_scores")
+    hbm_bytes = t1 if t1 is not None else b1
+    stage1 = {"kernels": "scores_kernel + select_kernel (bfla_estimate_mask)",
+              "ms": round(st1, 4), "flop": f1,
+              "achieved_tflops": round(f1 / (st1 * 1e-3) / 1e12, 2),
+              "mfma_frac": round(f1 / (st1 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+              "algorithmic_bytes": b1, "traffic": t1,
+              "hbm_gbs": round(hbm_bytes / (st1 * 1e-3) / 1e9, 1),
+              "hbm_bytes_source": "rocprofv3 FETCH+WRITE (profiles/)" if t1 is not None
+              else "algorithmic (Q and K once)",
+              "hbm_frac": round(hbm_bytes / (st1 * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+              "arithmetic_intensity": round(f1 / b1, 1),
+              "bound": "mfma" if f1 / b1 > PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"}
+
     config = {"workload": wl.name, "seq_lens": inp.n, "h_q": wl.h_q, "h_kv": wl.h_kv,
               "head_dim": wl.head_dim, "block": wl.block, "group": wl.group,
               "tile": wl.tile, "gamma": wl.gamma, "n_local": wl.n_local,
@@ -356,14 +422,17 @@ def main():
                      "traffic": measured_traffic(wl.name),
                      "flop_per_launch": flop_kept,
                      "launch_ms": round(pre_ms, 3)},
+        "stage1_roofline": stage1,
         "wall_s_timed": round(wall, 3),
         "input_gen_s": round(t_gen, 1),
     }
     if not args.no_cpu:
-        cpu, err = cpu_baseline(wl, inp, inp.o, args.cpu_seconds)
+        cpu, err, mchk = cpu_baseline(wl, inp, inp.o, args.cpu_seconds,
+                                      gpu_mask=buf.block_mask.cpu().numpy())
         log(f"cpu baseline {cpu['seconds']:.1f} s")
         result["cpu_baseline"] = {kk: vv for kk, vv in cpu.items() if kk != "seconds"}
         result["rel_err_vs_oracle_sampled"] = {kk: round(vv, 6) for kk, vv in err.items()}
+        result["mask_vs_oracle_sampled"] = mchk
     print(json.dumps(result), flush=True)
 
 

@@ -56,3 +56,36 @@ def test_more_than_one_gpu_is_refused():
     assert out.returncode == 2
     msg = json.loads(out.stdout.strip().splitlines()[-1])
     assert "one GPU" in msg["error"]
+
+
+def test_stage1_work_closed_form():
+    # N_c = 0, N a multiple of b: L (L + 1) / 2 causal block pairs per query
+    # head, G^2 group pairs each, 2 g C FLOP per group pair
+    n, b, g, c, h_q, h_kv = 128 * 10, 128, 64, 128, 8, 2
+    L, G = n // b, b // g
+    flop, nbytes = bench.stage1_work([n], [n], h_q, h_kv, c, b, g)
+    assert flop == 2.0 * g * c * G * G * h_q * L * (L + 1) // 2
+    assert nbytes == 2.0 * c * (h_q + h_kv) * n
+
+
+def test_stage1_work_counts_causal_pairs_by_brute_force():
+    # chunked prefill and a ragged tail: a block pair is causal when the KV
+    # block's first key is at or before the query block's last position
+    b, g = 128, 64
+    for n_kv, n_q in ((1000, 1000), (1000, 300), (777, 1)):
+        n_c = n_kv - n_q
+        pairs = 0
+        for i in range(-(-n_q // b)):
+            last = min(n_c + (i + 1) * b - 1, n_kv - 1)
+            pairs += sum(1 for j in range(-(-n_kv // b)) if j * b <= last)
+        flop, _ = bench.stage1_work([n_kv], [n_q], 1, 1, 64, b, g)
+        assert flop == 2.0 * g * 64 * (b // g) ** 2 * pairs
+
+
+def test_committed_score_traffic_matches_the_score_kernel_source():
+    for wl in ("llama_128k", "llama_32k", "wide_64k", "paged_4x"):
+        path = os.path.join(ROOT, "profiles", "prefill_" + wl.replace("_", "") + "_traffic.md")
+        if not os.path.exists(path):
+            continue
+        t = bench.measured_traffic(wl, "traffic_bytes_scores")
+        assert t is not None and t > 0, f"{wl}: stale or unreadable score-kernel traffic"
