@@ -89,3 +89,31 @@ def test_committed_score_traffic_matches_the_score_kernel_source():
             continue
         t = bench.measured_traffic(wl, "traffic_bytes_scores")
         assert t is not None and t > 0, f"{wl}: stale or unreadable score-kernel traffic"
+
+
+def test_sampled_mask_check_counts_sure_and_tie_mismatches():
+    # the bench's oracle leg compares the GPU block mask on the block rows it
+    # samples: fed the oracle's own mask it finds no mismatch; a flipped sure
+    # cell is counted as a sure mismatch
+    import numpy as np
+    import torch
+    from oracle import bfla_oracle as O
+    from paper_2605_12193_amd import synth
+    wl = synth.workload("tiny_2k")
+    seqs = synth.make_inputs(wl)
+    n = seqs[0].q.shape[1]
+    q, k = (t.double().numpy() for t in (seqs[0].q, seqs[0].k))
+    st = O.estimate_mask(q, k, wl.block, wl.group, wl.gamma, O.default_scale(wl.head_dim))
+
+    class Inp:
+        pass
+    inp = Inp()
+    inp.seqs, inp.n = seqs, [n]
+    out = torch.zeros(wl.h_q, n, wl.head_dim, dtype=torch.bfloat16)
+    inp.out_rows = lambda o, r, p, t0, t1: o[p, t0:t1].float().numpy()
+    mask = st["mask"].reshape(-1).astype(np.uint8)
+    _, _, m = bench.cpu_baseline(wl, inp, out, 1.0, gpu_mask=mask)
+    assert m["block_rows"] > 0 and m["sure_mismatch"] == 0 and m["tie_mismatch"] == 0
+    bad = 1 - mask   # every cell flipped: every sampled sure cell now differs
+    _, _, m2 = bench.cpu_baseline(wl, inp, out, 1.0, gpu_mask=bad)
+    assert m2["sure_mismatch"] == m2["blocks"] - m2["tie_blocks"] > 0
