@@ -199,7 +199,9 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params,
  *   row_ptr, cols  out, device int32 (layout above).
  *   cols_capacity  entries available at cols; must be >= max_cols of
  *                  bfla_list_capacity (else CAPACITY).
- *   workspace      device scratch of >= bfla_workspace_size(BFLA_WS_EXPAND).
+ *   workspace      device scratch of >= bfla_workspace_size(BFLA_WS_EXPAND),
+ *                  8-byte aligned (else INVALID_ARG); holds per-row counts and
+ *                  the keep / drop bits of every causal tile between passes.
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, CAPACITY, HIP. */
 int bfla_expand_rescue(const bfla_problem* prob, const bfla_params* params,
                        const uint8_t* block_mask, int32_t* row_ptr,

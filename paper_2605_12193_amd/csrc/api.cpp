@@ -48,6 +48,7 @@ struct Sizes {
   int64_t mask_bytes = 0;  // block mask
   int64_t score_elems = 0; // block scores
   int64_t lse_elems = 0;
+  int64_t max_t_kv = 0;    // KV tiles of the longest request
 };
 
 int64_t causal_tiles(int n_q, int n_kv, int T) {
@@ -111,6 +112,7 @@ Sizes sizes_of(const bfla_problem* prob, const bfla_params* pr) {
     s.mask_bytes += prob->h_kv * lq * lkv;
     s.score_elems += prob->h_q * lq * lkv;
     s.lse_elems += (int64_t)prob->h_q * nq;
+    s.max_t_kv = std::max<int64_t>(s.max_t_kv, cdiv(nkv, pr->tile));
   }
   return s;
 }
@@ -317,7 +319,7 @@ int bfla_workspace_size(const bfla_problem* prob, const bfla_params* params, int
   if (which == BFLA_WS_ESTIMATE) {
     *bytes = (size_t)s.score_elems * sizeof(float);
   } else if (which == BFLA_WS_EXPAND) {
-    *bytes = expand_workspace_bytes(s.n_rows);
+    *bytes = expand_workspace_bytes(s.n_rows, s.max_t_kv);
   } else {
     return fail(BFLA_ERR_INVALID_ARG, "unknown workspace kind %d", which);
   }
@@ -386,15 +388,19 @@ int bfla_expand_rescue(const bfla_problem* prob, const bfla_params* params,
   if (cols_capacity < (size_t)s.max_cols)
     return fail(BFLA_ERR_CAPACITY, "cols capacity %zu < %lld causal tiles", cols_capacity,
                 (long long)s.max_cols);
-  size_t need = expand_workspace_bytes(s.n_rows);
+  size_t need = expand_workspace_bytes(s.n_rows, s.max_t_kv);
   if (!workspace || ws_bytes < need)
     return fail(BFLA_ERR_WORKSPACE, "expand workspace %zu < %zu bytes", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 7)
+    return fail(BFLA_ERR_INVALID_ARG, "expand workspace not 8-byte aligned");
   ExpandLaunch L{};
   L.block_mask = block_mask;
   L.row_ptr = row_ptr;
   L.cols = cols;
   L.counts = static_cast<int32_t*>(workspace);
   L.partial = L.counts + ((s.n_rows + 63) / 64) * 64;
+  L.words_per_row = (int32_t)((s.max_t_kv + 63) / 64);
+  L.bits = reinterpret_cast<uint64_t*>(L.partial + 64);
   L.n_rows = (int32_t)s.n_rows;
   L.h_kv = prob->h_kv;
   L.rb = params->block / params->tile;

@@ -29,6 +29,8 @@ struct ExpandLaunch {
   int32_t* cols;
   int32_t* counts;   // workspace [n_rows]
   int32_t* partial;  // workspace [scan blocks]
+  uint64_t* bits;    // workspace [n_rows][words_per_row]: keep ballots of 64 tiles
+  int32_t words_per_row;
   int32_t n_rows;
   int32_t h_kv;
   int32_t rb;        // b / T
@@ -39,7 +41,7 @@ struct ExpandLaunch {
 };
 
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream);
-size_t expand_workspace_bytes(int64_t n_rows);
+size_t expand_workspace_bytes(int64_t n_rows, int64_t max_t_kv);
 
 struct EstimateLaunch {
   const void* q;

@@ -7,8 +7,10 @@
 //           | sink kt < n_sink                            (eq22)
 //   rescued = !kept & (chi(qt, kt; s) mod eta == 0        (eq24)
 //                      | psi(h, qt, kt; s) < rho)         (eq25)
-// and the wave ballot gives counts (pass 1) or list positions (pass 3).
-// Pass 2 is an exclusive scan of the row counts in one workgroup.
+// Pass 1 stores the wave ballots (one 64-bit word per 64 tiles of a row) and
+// the row counts; pass 2 is an exclusive scan of the counts in one
+// workgroup; pass 3 reads the ballots back and writes each kept tile at its
+// list position, so every keep / drop decision is taken once.
 #include "bfla_device.h"
 #include "bfla_internal.h"
 
@@ -24,9 +26,12 @@ struct ExpandArgs {
   int32_t* row_ptr;
   int32_t* cols;
   int32_t* counts;
+  uint64_t* bits;
+  int32_t words_per_row;
   int32_t n_rows;
   int32_t h_kv, rb;
   int32_t n_local, n_sink, eta;
+  uint32_t eta_mask;  // eta - 1 when eta is a power of two, else 0
   uint32_t rho24;
   uint64_t chi_key;  // mix64(s)
   uint64_t psi_key;  // mix64(s + 1)
@@ -70,7 +75,12 @@ __device__ __forceinline__ bool keep_tile(const ExpandArgs& a, const RowCtx& c, 
   kept |= kt < a.n_sink;
   if (kept) return true;
   const uint64_t key = ((uint64_t)c.qt << 21) | (uint64_t)kt;
-  if (a.eta > 0 && (mix64(a.chi_key ^ key) % (uint64_t)a.eta) == 0) return true;
+  if (a.eta > 0) {
+    // chi mod eta == 0; for a power-of-two eta the low bits decide it (the
+    // same test without a 64-bit division)
+    const uint64_t chi = mix64(a.chi_key ^ key);
+    if (a.eta_mask != 0 ? (chi & a.eta_mask) == 0 : chi % (uint64_t)a.eta == 0) return true;
+  }
   if (a.rho24 > 0) {
     uint64_t hk = key | ((uint64_t)(c.h + 1) << 42);
     if ((uint32_t)(mix64(a.psi_key ^ hk) >> 40) < a.rho24) return true;
@@ -83,9 +93,11 @@ __global__ void __launch_bounds__(64 * ROWS_PER_WG) count_kernel(ExpandArgs a) {
   const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
   RowCtx c;
   if (!row_ctx(a, row, &c)) return;
+  uint64_t* bits = a.bits + (int64_t)row * a.words_per_row;
   int total = 0;
   for (int k0 = 0; k0 < c.n_tiles; k0 += 64) {
-    unsigned long long b = __ballot(keep_tile(a, c, k0 + lane));
+    const uint64_t b = __ballot(keep_tile(a, c, k0 + lane));
+    if (lane == 0) bits[k0 >> 6] = b;
     total += __popcll(b);
   }
   if (lane == 0) a.counts[row] = total;
@@ -129,11 +141,12 @@ __global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a)
   const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
   RowCtx c;
   if (!row_ctx(a, row, &c)) return;
+  const uint64_t* bits = a.bits + (int64_t)row * a.words_per_row;
   int pos = a.row_ptr[row];
   for (int k0 = 0; k0 < c.n_tiles; k0 += 64) {
     const int kt = k0 + lane;
-    const bool keep = keep_tile(a, c, kt);
-    unsigned long long b = __ballot(keep);
+    const uint64_t b = bits[k0 >> 6];   // pass 1's ballot of these 64 tiles
+    const bool keep = (b >> lane) & 1;
     int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
                                            __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0));
     if (keep) a.cols[pos + before] = kt;
@@ -143,8 +156,11 @@ __global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a)
 
 }  // namespace
 
-size_t expand_workspace_bytes(int64_t n_rows) {
-  return (size_t)(((n_rows + 63) / 64) * 64 + 64) * sizeof(int32_t);
+// counts [n_rows rounded up to 64] + scan partials [64] (int32), then the
+// ballots [n_rows][ceil(max_t_kv / 64)] (uint64, 256-byte aligned offset)
+size_t expand_workspace_bytes(int64_t n_rows, int64_t max_t_kv) {
+  return (size_t)(((n_rows + 63) / 64) * 64 + 64) * sizeof(int32_t) +
+         (size_t)n_rows * (size_t)((max_t_kv + 63) / 64) * sizeof(uint64_t);
 }
 
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
@@ -154,12 +170,15 @@ hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
   a.row_ptr = L.row_ptr;
   a.cols = L.cols;
   a.counts = L.counts;
+  a.bits = L.bits;
+  a.words_per_row = L.words_per_row;
   a.n_rows = L.n_rows;
   a.h_kv = L.h_kv;
   a.rb = L.rb;
   a.n_local = L.n_local;
   a.n_sink = L.n_sink;
   a.eta = L.eta;
+  a.eta_mask = (L.eta > 1 && (L.eta & (L.eta - 1)) == 0) ? (uint32_t)(L.eta - 1) : 0u;
   a.rho24 = L.rho24;
   a.chi_key = mix64(L.seed);
   a.psi_key = mix64(L.seed + 1);

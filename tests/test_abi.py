@@ -120,6 +120,10 @@ def test_entry_points_reject_before_launch():
     st = L.bfla_expand_rescue(C.byref(p.c), C.byref(prm), addr, addr, addr, 1 << 20, addr, 0,
                               None)
     assert st == bfla.BFLA_ERR_WORKSPACE
+    # expand workspace not 8-byte aligned
+    st = L.bfla_expand_rescue(C.byref(p.c), C.byref(prm), addr, addr, addr, 1 << 20,
+                              C.c_void_p((1 << 20) + 4), 1 << 30, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
     # misaligned q
     bad = bfla.bfla_view((1 << 20) + 2, None, 0, 256 * 64, 64)
     st = L.bfla_sparse_prefill(C.byref(p.c), C.byref(prm), C.byref(bad), C.byref(kv), addr,
@@ -173,3 +177,15 @@ def test_estimate_address_limits():
                               None, 0, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
     assert "pages" in L.bfla_last_error().decode()
+
+
+def test_expand_workspace_holds_counts_and_ballots():
+    # per-row counts and scan partials (int32), then one 64-bit keep ballot per
+    # 64 KV tiles of the longest request for every list row
+    prm = bfla.params()
+    for n_q, n_kv in (([4096], [4096]), ([300, 5000], [1000, 5000]), ([64], [64])):
+        p = bfla.Problem(n_q, n_kv, 8, 2, 128)
+        cap = bfla.bfla_list_capacity(p, prm)
+        words = -(-max(-(-n // 64) for n in n_kv) // 64)
+        want = (-(-cap.n_rows // 64) * 64 + 64) * 4 + cap.n_rows * words * 8
+        assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) == want
