@@ -119,6 +119,11 @@ def test_sparse_prefill_empty_rows_and_band_off():
     dict(n_local=0, n_sink=3, eta=3, rho=0.0),
     dict(n_local=5, n_sink=1, eta=0, rho=1.0),
     dict(block=256, n_local=8, eta=16, rho=0.37, seed=123456789),
+    # the stride test on the low bits of chi (eta a power of two) and by
+    # division (other eta), and eta = 1 rescuing every dropped tile
+    dict(n_local=0, n_sink=0, eta=1, rho=0.0),
+    dict(n_local=1, eta=2, rho=0.0, seed=99),
+    dict(n_local=1, eta=12, rho=0.05, seed=7),
 ])
 @pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[4], SHAPES[8]], ids=["tiny", "chunked", "batch3"])
 def test_expand_rescue_bit_exact(shape, cfg):
