@@ -34,6 +34,7 @@
 // taken, the running max moves up to it where it is larger (O and l
 // rescaled) and the weights are recomputed (all <= 1).  O and l always refer
 // to the same max, so O / l is exact.
+#include <atomic>
 #include <utility>
 
 #include "bfla_device.h"
@@ -685,12 +686,18 @@ hipError_t launch_one(const PrefillArgs& a, int n_work, hipStream_t s) {
   auto kern = prefill_kernel<C, M, DENSE, PAGED>;
   constexpr int lds = Cfg<C>::LDS_BYTES;
   static_assert(lds <= 160 * 1024, "LDS budget");
-  static bool attr_set = false;  // idempotent; a benign race sets it twice
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  // The dynamic-LDS limit is raised once per device (bit d of the mask);
+  // setting it is idempotent, so two threads racing on a device both set it.
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? uint64_t(1) << dev : 0;
+  if (!bit || !(attr_set.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_set.fetch_or(bit, std::memory_order_release);
   }
   hipLaunchKernelGGL(kern, dim3(n_work), dim3(64 * Shape<C, M>::WAVES), lds, s, a);
   return hipGetLastError();
