@@ -8,36 +8,9 @@ import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import DeviceBatch, compare_outputs, mask_compare
+from parity_util import DeviceBatch, PagedBatch, compare_outputs, mask_compare
 
 pytestmark = pytest.mark.gpu
-
-
-class PagedBatch:
-    """Packed token-major Q/O [sum N_q][H_q][C]; K/V in page pools."""
-
-    def __init__(self, seqs, n_q, page_size, seed):
-        self.n_kv = [s.k.shape[1] for s in seqs]
-        self.n_q = list(n_q)
-        h_q, _, c = seqs[0].q.shape
-        h_kv = seqs[0].k.shape[0]
-        qs = [s.q[:, s.q.shape[1] - nq:].transpose(0, 1) for s, nq in zip(seqs, self.n_q)]
-        self.q = torch.cat(qs, dim=0).contiguous().cuda()          # [sum N_q][H_q][C]
-        self.o = torch.full_like(self.q, float("nan"))
-        starts = np.concatenate([[0], np.cumsum(self.n_q)[:-1]]).astype(int)
-        table, total = synth.page_table(seed, self.n_kv, page_size)
-        kp, vp = synth.to_paged(seqs, table, total, page_size)
-        self.kp, self.vp = kp.cuda(), vp.cuda()
-        self.table = torch.from_numpy(table).cuda()
-        self.prob = bfla.Problem(self.n_q, self.n_kv, h_q, h_kv, c)
-        self.qv = bfla.view_packed(self.q, starts)
-        self.ov = bfla.view_packed(self.o, starts)
-        self.kv = bfla.KV(self.kp, self.vp, paged=True, block_table=self.table)
-        self.starts = starts
-
-    def o_of(self, r):
-        a = self.starts[r]
-        return self.o[a:a + self.n_q[r]].transpose(0, 1).float().cpu().numpy()
 
 
 SHAPES = [
