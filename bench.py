@@ -386,6 +386,8 @@ def main():
               "arithmetic_intensity": round(f1 / b1, 1),
               "bound": "mfma" if f1 / b1 > PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"}
 
+    traffic = measured_traffic(wl.name)
+
     config = {"workload": wl.name, "seq_lens": inp.n, "h_q": wl.h_q, "h_kv": wl.h_kv,
               "head_dim": wl.head_dim, "block": wl.block, "group": wl.group,
               "tile": wl.tile, "gamma": wl.gamma, "n_local": wl.n_local,
@@ -419,9 +421,13 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "prefill_kernel (sparse)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(wl.name),
+                     "traffic": traffic,
                      "flop_per_launch": flop_kept,
-                     "launch_ms": round(pre_ms, 3)},
+                     "launch_ms": round(pre_ms, 3),
+                     # the other roofline: measured HBM bytes over the same launch time
+                     "hbm_gbs": None if traffic is None else round(traffic / (pre_ms * 1e-3) / 1e9, 1),
+                     "hbm_frac": None if traffic is None else
+                     round(traffic / (pre_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
         "stage1_roofline": stage1,
         "wall_s_timed": round(wall, 3),
         "input_gen_s": round(t_gen, 1),
