@@ -24,7 +24,7 @@ def draw(i):
     rng = np.random.default_rng(2026 + i)
     c = int(rng.choice([64, 128, 256], p=[0.4, 0.4, 0.2]))
     h_kv = int(rng.choice([1, 2]))
-    m = int(rng.integers(1, 9)) if c < 256 else int(rng.integers(1, 3))
+    m = int(rng.integers(1, 9))
     block = int(rng.choice([64, 128, 256]))
     G = int(rng.choice([x for x in (1, 2, 4, 8, 16) if block // x >= 4]))
     batch = int(rng.choice([1, 1, 2, 3]))

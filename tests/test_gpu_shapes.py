@@ -2,16 +2,18 @@
 the oracle: C in {64, 128, 256} x m in 1..8.  Each runs a ragged
 333-token request (five full tiles and a 13-token tail) through the sparse
 prefill on the oracle's own lists and through the dense prefill.  This covers
-the ping-pong shapes (m = 4, 8 at C <= 128), the two-stage shapes and the
-half-tile shapes (m > 4 at C <= 128, m > 2 at C = 256), including those whose
-registers spill (C = 256 with m = 1 or m > 2)."""
+the ping-pong shapes (m = 4, 8 at C <= 128), the two-stage shapes, the
+half-tile shapes (m > 4 at C <= 128) and, at C = 256, the 16-query kernels
+over whole (m <= 2), half (m = 3, 4) and quarter (m >= 5) q-tiles.  The
+paged cases run the same shapes on K/V in 16-token pages with two KV heads."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import DeviceBatch, compare_outputs, lists_to_device, oracle_lists_for
+from parity_util import (DeviceBatch, PagedBatch, compare_outputs, lists_to_device,
+                         oracle_lists_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -61,4 +63,35 @@ def test_dense_shape(c, m):
     q, k, v = db.host(0)
     want, want_lse = O.attention(q, k, v, 64, O.default_scale(c))
     compare_outputs(db.o_of(0), want, f"dense C={c} m={m}")
+    _check_lse(lse.cpu().numpy(), want_lse)
+
+
+PAGED_CASES = [(256, m) for m in range(1, 9)] + [(128, 1), (128, 4), (128, 5), (64, 8)]
+
+
+@pytest.mark.parametrize("c,m", PAGED_CASES, ids=[f"c{c}_m{m}" for c, m in PAGED_CASES])
+def test_paged_shape(c, m):
+    """Sparse (oracle lists) and dense prefill on paged K/V, two KV heads."""
+    wl = synth.workload("tiny_2k", h_q=2 * m, h_kv=2, head_dim=c, seed=200 + c + m)
+    seqs = synth.make_inputs(wl, seqlens=[N])
+    pb = PagedBatch(seqs, [N], page_size=16, seed=7 + m)
+    kw, prm = _params()
+    s = seqs[0]
+    q, k, v = s.q.double().numpy(), s.k.double().numpy(), s.v.double().numpy()
+    alpha = O.default_scale(c)
+    masks = O.estimate_mask(q, k, kw["block"], kw["group"], kw["gamma"], alpha)["mask"]
+    rp, cols, _ = O.expand_rescue([masks], [N], [N], kw["block"], kw["tile"], kw["n_local"],
+                                  kw["n_sink"], kw["eta"], kw["rho"], kw["seed"])
+    drp, dcols = lists_to_device(rp, cols)
+    lse = torch.full((2 * m * N,), float("nan"), device="cuda")
+    bfla.bfla_sparse_prefill(pb.prob, prm, pb.qv, pb.kv, drp, dcols, pb.ov, lse)
+    torch.cuda.synchronize()
+    want, want_lse = O.attention(q, k, v, 64, alpha, rp, cols, 0)
+    compare_outputs(pb.o_of(0), want, f"paged sparse C={c} m={m}")
+    _check_lse(lse.cpu().numpy(), want_lse)
+    lse.fill_(float("nan"))
+    bfla.bfla_dense_prefill(pb.prob, prm, pb.qv, pb.kv, pb.ov, lse)
+    torch.cuda.synchronize()
+    want, want_lse = O.attention(q, k, v, 64, alpha)
+    compare_outputs(pb.o_of(0), want, f"paged dense C={c} m={m}")
     _check_lse(lse.cpu().numpy(), want_lse)
