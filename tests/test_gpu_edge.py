@@ -61,21 +61,27 @@ def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
         compare_outputs(db.o_of(r), want, f"dense request {r} of {len(seqs)}")
 
 
-# (C, H_q): C = 256 with GQA 2 runs the 16-query ping-pong kernel
-@pytest.mark.parametrize("c,h_q", [(64, 4), (256, 4)], ids=["c64", "c256_gqa2"])
+# (C, H_q) with two KV heads: C = 256 with GQA 2 runs the 16-query ping-pong
+# kernel; GQA 1 and 5 the 16-query kernel over whole and quarter q-tiles
+SHAPES = [(64, 4), (256, 4), (256, 2), (256, 10)]
+SHAPE_IDS = ["c64", "c256_gqa2", "c256_gqa1", "c256_gqa5"]
+
+
+@pytest.mark.parametrize("c,h_q", SHAPES, ids=SHAPE_IDS)
 @pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 127, 128, 129])
 def test_short_sequences(n, c, h_q):
     _run([n], h_q=h_q, c=c)
 
 
-@pytest.mark.parametrize("c,h_q", [(64, 8), (128, 8), (256, 4)], ids=["c64", "c128", "c256_gqa2"])
+@pytest.mark.parametrize("c,h_q", [(64, 8), (128, 8)] + SHAPES[1:],
+                         ids=["c64", "c128"] + SHAPE_IDS[1:])
 def test_single_query_after_long_prefix(c, h_q):
     _run([1000], n_q=[1], h_q=h_q, h_kv=2, c=c)
 
 
-@pytest.mark.parametrize("c", [64, 256], ids=["c64", "c256_gqa2"])
-def test_max_batch_of_32_requests(c):
+@pytest.mark.parametrize("c,h_q", SHAPES, ids=SHAPE_IDS)
+def test_max_batch_of_32_requests(c, h_q):
     rng = np.random.default_rng(3)
     seqlens = [int(x) for x in rng.integers(1, 700, size=32)]
     n_q = [max(1, int(n * f)) for n, f in zip(seqlens, rng.uniform(0.3, 1.0, size=32))]
-    _run(seqlens, n_q=n_q, c=c)
+    _run(seqlens, n_q=n_q, h_q=h_q, c=c)

@@ -11,8 +11,8 @@ from paper_2605_12193_amd import bfla, synth
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("h_q,h_kv,c", [(8, 2, 128), (4, 2, 256), (10, 2, 128)],
-                         ids=["pingpong_gqa4", "two_stage_c256", "half_tile_gqa5"])
+@pytest.mark.parametrize("h_q,h_kv,c", [(8, 2, 128), (4, 2, 256), (10, 2, 128), (6, 2, 256)],
+                         ids=["pingpong_gqa4", "wide_c256", "half_tile_gqa5", "q16_c256_gqa3"])
 def test_sparse_pass_graph_replays_match_eager(h_q, h_kv, c):
     n = 4608 + 37
     prob = bfla.Problem([n], [n], h_q, h_kv, c)
