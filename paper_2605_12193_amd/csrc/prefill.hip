@@ -27,12 +27,11 @@
 //
 // The lane ^ 32 exchanges of the row max and sum use v_permlane32_swap.
 //
-// Head dim 256 runs on 16-query waves (v_mfma_f32_16x16x32_bf16) instead.
-// GQA 2 runs prefill_wide_kernel: the same ping-pong, with K and V in
-// separate two-slot rings offset by one tile (three combined stages of 256
-// channels would not fit the LDS).  Every other group size runs
-// prefill_q16_kernel: all of a work item's waves in the same phase, over a
-// whole, half or quarter q-tile so that it has at most 8 waves.
+// Head dim 256 runs prefill_q16_kernel instead: 16-query waves on
+// v_mfma_f32_16x16x32_bf16 over a whole, half or quarter q-tile (at most 8
+// waves), K and V in separate two-slot rings offset by one tile (three
+// combined stages of 256 channels would not fit the LDS); the same ping-pong
+// at GQA 2, all waves in one phase otherwise.
 //
 // The online softmax keeps a stale running max and takes no max reduction in
 // the common case: a tile's weights are computed against the running max and
@@ -183,10 +182,10 @@ __device__ __forceinline__ void lgkm_wait(u32x4& r) {
 // than two waves on a SIMD).
 __host__ __device__ constexpr bool half_shape(int c, int m) { return m > 4; }
 // Head dim 256 runs on 16-query waves (a 32-query wave's 256-channel O, Q and
-// S would leave one wave per SIMD): prefill_wide_kernel for GQA 2,
-// prefill_q16_kernel otherwise.  A q16 work item covers QB
-// 16-query blocks of one q-tile for all m heads, so that it has m * QB <= 8
-// waves: the whole tile at m <= 2, half at m = 3, 4, a quarter at m >= 5.
+// S would leave one wave per SIMD), prefill_q16_kernel.  A work item covers
+// QB 16-query blocks of one q-tile for all m heads, so that it has
+// m * QB <= 8 waves: the whole tile at m <= 2, half at m = 3, 4, a quarter
+// at m >= 5.
 __host__ __device__ constexpr int q16_blocks(int m) { return m <= 2 ? 4 : m <= 4 ? 2 : 1; }
 // work items per list row (request, KV head, q-tile)
 __host__ __device__ constexpr int parts_per_row(int c, int m) {
@@ -775,13 +774,7 @@ __device__ __forceinline__ KvTiles<PAGED> kv_tiles(const PrefillArgs& a, const R
   return kt;
 }
 
-// ---- C = 256, GQA 2: ping-pong over 16-query waves ----
-// Eight waves of 16 queries (v_mfma_f32_16x16x32_bf16), group A = head 0 of
-// the pair (waves 0-3), group B = head 1 (waves 4-7), one wave of each per
-// SIMD.  K and V live in separate two-slot rings offset by one tile: in the
-// phases of iteration i the streams read K(i+1) and V(i), while K(i+2) and
-// V(i+1) are staged into the other slots (141 KiB of LDS instead of the
-// 212 KiB three combined stages would take).
+// ---- head dim 256: 16-query waves on v_mfma_f32_16x16x32_bf16 ----
 __device__ __forceinline__ f32x4 mfma16x16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
@@ -806,332 +799,27 @@ __device__ __forceinline__ int vperm16(int k) {
   return (k & 32) | (((k >> 2) & 3) << 3) | (((k >> 4) & 1) << 2) | (k & 3);
 }
 
-template <bool DENSE, bool PAGED>
-__global__ void __launch_bounds__(512) prefill_wide_kernel(PrefillArgs a) {
-  constexpr int C = 256, NT = 512;
-  constexpr int KROW = C + 8, VROW = TILE + 8;
-  constexpr int K_SLOT = TILE * KROW, V_SLOT = C * VROW;
-  constexpr int KC_PER_T = (TILE * C / 8) / NT;          // 4 chunks of 8 channels
-  constexpr int VU_PER_T = ((TILE / 2) * (C / 8)) / NT;  // 2 (key pair x 8 channels)
-  constexpr int NKC = C / 32, NCB = C / 16;              // 8 chunks, 16 blocks
-  extern __shared__ __align__(16) bf16_t lds[];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int l16 = lane & 15;
-  const int g = lane >> 4;
-
-  const int w = blockIdx.x;
-  const int ri = find_req(a.batch, w);
-  const ReqDesc& Rd = a.batch.r[ri];
-  const int n_q = Rd.n_q, n_kv = Rd.n_kv, t_q = Rd.t_q, t_kv = Rd.t_kv;
-  const int64_t q_off = Rd.q_off, o_off = Rd.o_off, kv_off = Rd.kv_off, lse_off = Rd.lse_off;
-  const int local = w - Rd.work_begin;
-  const int h = local % a.h_kv;
-  const int qt = t_q - 1 - local / a.h_kv;
-  const int row = Rd.row_base + h * t_q + qt;
-  const int n_c = n_kv - n_q;
-  int list_begin = 0, n_tiles;
-  if (DENSE) {
-    n_tiles = min(n_c + (qt + 1) * TILE - 1, n_kv - 1) / TILE + 1;
-  } else {
-    list_begin = uniform_load(a.row_ptr, row);
-    n_tiles = uniform_load(a.row_ptr, row + 1) - list_begin;
-  }
-  const int p = h * 2 + (wave >> 2);
-  const int t = qt * TILE + (wave & 3) * 16 + l16;     // this lane's query
-  const int wave_q0 = n_c + qt * TILE + (wave & 3) * 16;
-
-  bf16x8 qf[NKC];
-  {
-    const bf16_t* qp = a.q + q_off + (int64_t)p * a.q_sh + (int64_t)t * a.q_st + 8 * g;
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      qf[kc] = as_bf16x8(t < n_q ? ld16(qp + 32 * kc) : make_uint4(0, 0, 0, 0));
-  }
-  __builtin_amdgcn_s_waitcnt(VMCNT0);
-
-  __amdgpu_buffer_rsrc_t krs, vrs;
-  const KvTiles<PAGED> kvt = kv_tiles<C, PAGED>(a, Rd, h, krs, vrs);
-  const int64_t st = a.kv.stride_tok;
-  int k_row[KC_PER_T], k_ce[KC_PER_T];
-  uint32_t k_boff[KC_PER_T];
-#pragma unroll
-  for (int i = 0; i < KC_PER_T; ++i) {
-    const int e = tid + i * NT;
-    k_row[i] = e / (C / 8);
-    k_ce[i] = e % (C / 8);
-    k_boff[i] = (uint32_t)(((int64_t)k_row[i] * st + 8 * k_ce[i]) * 2);
-  }
-  int v_j[VU_PER_T], v_ce[VU_PER_T];
-  uint32_t v_boff[VU_PER_T];
-#pragma unroll
-  for (int i = 0; i < VU_PER_T; ++i) {
-    const int u = tid + i * NT;
-    v_j[i] = u % (TILE / 2);
-    v_ce[i] = u / (TILE / 2);
-    v_boff[i] = (uint32_t)(((int64_t)(2 * v_j[i]) * st + 8 * v_ce[i]) * 2);
-  }
-  const uint32_t st_bytes = (uint32_t)(st * 2);
-  struct KSet { uint4 k[KC_PER_T]; };
-  struct VSet { uint4 v[VU_PER_T][2]; };
-  // paged: the page numbers are read where the fetch is issued (taking them
-  // out of the streams keeps 8 more VGPRs live across the loop, which spill)
-  auto load_k = [&](int kt, KSet& sk) INLINE {
-    const TileAt at = kvt.locate(kt);
-#pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) sk.k[i] = bload16(krs, kvt.off(at, k_row[i], k_ce[i], k_boff[i]));
-  };
-  auto load_v = [&](int kt, VSet& sv) INLINE {
-    const TileAt at = kvt.locate(kt);
-#pragma unroll
-    for (int i = 0; i < VU_PER_T; ++i) {
-      sv.v[i][0] = bload16(vrs, kvt.off(at, 2 * v_j[i], v_ce[i], v_boff[i]));
-      sv.v[i][1] = bload16(vrs, kvt.off(at, 2 * v_j[i] + 1, v_ce[i], v_boff[i] + st_bytes));
-    }
-  };
-  bf16_t* const kring = lds;                  // [2][K_SLOT]
-  bf16_t* const vring = lds + 2 * K_SLOT;     // [2][V_SLOT]
-  auto store_k = [&](int slot, const KSet& sk, int i) INLINE {
-    *reinterpret_cast<uint4*>(kring + slot * K_SLOT + k_row[i] * KROW + 8 * k_ce[i]) = sk.k[i];
-  };
-  auto store_v = [&](int slot, const VSet& sv, int i) INLINE {
-    const int pos = vperm16(2 * v_j[i]);
-    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sv.v[i][0]);
-    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sv.v[i][1]);
-    bf16_t* col = vring + slot * V_SLOT + 8 * v_ce[i] * VROW + pos;
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
-      const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
-      *reinterpret_cast<uint32_t*>(col + (2 * e2) * VROW) = lo;
-      *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * VROW) = hi2;
-    }
-  };
-  auto tile_or_none = [&](int i) INLINE -> int {
-    if (DENSE) return i < n_tiles ? i : -1;
-    const int tt = uniform_load(a.cols, __builtin_amdgcn_readfirstlane(list_begin + min(i, n_tiles - 1)));
-    return i < n_tiles ? tt : -1;
-  };
-
-  const float c2 = a.scale * LOG2E;
-  float m_run = -INFINITY, l_run = 0.f;
-  bool max_ok = false;
-  f32x4 acc[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  f32x4 sc[4];     // keys 16 kb + 4 g + r of the tile, this lane's query
-  bf16x8 pf[2];    // P^T B operands, 32-key chunks
-
-  constexpr int DEPTH = 4;
-  const uint32_t lds_base = LDS_ADDR(lds);
-  const uint32_t k_lane = lds_base + (uint32_t)((l16 * KROW + 8 * g) * 2);
-  const uint32_t v_lane = lds_base + (uint32_t)((2 * K_SLOT + l16 * VROW + 8 * g) * 2);
-  auto no_hook = [](auto) INLINE {};
-  // PV of the tile in V slot v_slot (P in pf) and/or QK of the tile in K slot
-  // k_slot (S into sc); one LDS fragment per MFMA, read DEPTH ahead
-  auto stream = [&](auto do_pv, auto do_qk, int v_slot, int k_slot, auto&& hook) INLINE {
-    constexpr int NV = decltype(do_pv)::value ? 2 * NCB : 0;   // (cb, 32-key chunk)
-    constexpr int NK = decltype(do_qk)::value ? 4 * NKC : 0;   // (kb, 32-channel chunk)
-    constexpr int N = NV + NK;
-    const uint32_t va = v_lane + (uint32_t)(v_slot * V_SLOT * 2);
-    const uint32_t ka = k_lane + (uint32_t)(k_slot * K_SLOT * 2);
-    u32x4 ring[DEPTH];
-    auto issue = [&](auto jc) INLINE {
-      constexpr int j = decltype(jc)::value;
-      if constexpr (j < NV)
-        lds_read<(16 * (j % NCB) * VROW + 32 * (j / NCB)) * 2>(ring[j % DEPTH], va);
-      else
-        lds_read<(16 * ((j - NV) & 3) * KROW + 32 * ((j - NV) >> 2)) * 2>(ring[j % DEPTH], ka);
-    };
-    static_for<(DEPTH < N ? DEPTH : N)>(issue);
-    const f32x4 zero = {};
-    static_for<N>([&](auto jc) INLINE {
-      constexpr int j = decltype(jc)::value;
-      lgkm_wait<(N - 1 - j < DEPTH - 1 ? N - 1 - j : DEPTH - 1)>(ring[j % DEPTH]);
-      const bf16x8 av = __builtin_bit_cast(bf16x8, ring[j % DEPTH]);
-      if constexpr (j < NV) {
-        acc[j % NCB] = mfma16x16(av, pf[j / NCB], acc[j % NCB]);
-      } else {
-        constexpr int kb = (j - NV) & 3;
-        sc[kb] = mfma16x16(av, qf[(j - NV) >> 2], (j - NV) < 4 ? zero : sc[kb]);
-      }
-      if constexpr (j + DEPTH < N) issue(std::integral_constant<int, j + DEPTH>{});
-      hook(jc);
-      __builtin_amdgcn_sched_barrier(0);
-    });
-  };
-  const std::true_type YES;
-  const std::false_type NO;
-
-  auto exp_pack = [&](float moff) INLINE -> float {
-    float r0 = 0.f, r1 = 0.f;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      uint32_t wd[4];
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const f32x4& v = sc[2 * c + hb];
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(v[0], c2, moff));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(v[1], c2, moff));
-        const float p2 = __builtin_amdgcn_exp2f(fmaf(v[2], c2, moff));
-        const float p3 = __builtin_amdgcn_exp2f(fmaf(v[3], c2, moff));
-        wd[2 * hb] = pack_bf16x2(p0, p1);
-        wd[2 * hb + 1] = pack_bf16x2(p2, p3);
-        r0 += p0;
-        r1 += p1;
-        r0 += p2;
-        r1 += p3;
-      }
-      pf[c] = as_bf16x8(make_uint4(wd[0], wd[1], wd[2], wd[3]));
-    }
-    return r0 + r1;
-  };
-  auto softmax = [&](int kt_s) INLINE {
-    const int key0 = kt_s * TILE;
-    if ((unsigned)kt_s >= (unsigned)t_kv || key0 + TILE - 1 > wave_q0 || key0 + TILE > n_kv) {
-      const int lim = ((unsigned)kt_s >= (unsigned)t_kv ? -1 : min(n_c + t, n_kv - 1)) - key0 - 4 * g;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sc[kb][r] = 16 * kb + r <= lim ? sc[kb][r] : -INFINITY;
-    }
-    bool done = false;
-    float rs = 0.f;
-    if (max_ok) {
-      rs = add_lane4(exp_pack(-m_run * c2));
-      done = !__builtin_amdgcn_ballot_w64(!(rs <= RESCALE_SUM));
-    }
-    if (!done) {
-      float x = sc[0][0];
-#pragma unroll
-      for (int i = 1; i < 16; ++i) x = fmaxf(x, sc[i / 4][i % 4]);
-      const float mx = max_lane4(x);
-      const bool grow = mx > m_run;
-      if (__builtin_amdgcn_ballot_w64(grow)) {
-        const float m_new = grow ? mx : m_run;
-        const float corr = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c2) : 1.f;
-        m_run = m_new;
-        l_run *= corr;
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[cb][r] *= corr;
-      }
-      max_ok = !__builtin_amdgcn_ballot_w64(m_run == -INFINITY);
-      rs = add_lane4(exp_pack((m_run == -INFINITY) ? 0.f : -m_run * c2));
-    }
-    l_run += rs;
-  };
-
-  if (n_tiles > 0) {
-    // sk holds the K part of tile i + 2, sv the V part of tile i + 1
-    KSet sk;
-    VSet sv;
-    int kt[5];   // tiles i .. i + 4
-#pragma unroll
-    for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
-    load_k(kt[0], sk);
-    load_v(kt[0], sv);
-#pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
-#pragma unroll
-    for (int i = 0; i < VU_PER_T; ++i) store_v(0, sv, i);
-    load_k(kt[1], sk);
-#pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) store_k(1, sk, i);
-    load_k(kt[2], sk);
-    load_v(kt[1], sv);
-    __syncthreads();
-    auto run = [&](auto is_a) INLINE {
-      constexpr bool A = decltype(is_a)::value;
-      if (A) stream(NO, YES, 0, 0, no_hook);
-      __syncthreads();
-      if (A) softmax(kt[0]);
-      else stream(NO, YES, 0, 0, no_hook);
-      __syncthreads();
-      int it = 0;
-      // iteration i (tile parity ip = i & 1): phases Y_i, X_i+1.  The streams
-      // read V(i) (V slot ip) and K(i+1) (K slot 1 - ip); each thread stages
-      // its K chunks of tile i + 2 into K slot ip between the MFMAs of its
-      // stream and then fetches those of tile i + 3, and in its softmax phase
-      // stores its V units of tile i + 1 into V slot 1 - ip and fetches those
-      // of tile i + 2.
-      auto iteration = [&](auto ipc) INLINE {
-        constexpr int ip = decltype(ipc)::value;
-        const int kt_k = kt[3], kt_v = kt[2];
-        auto stage_hook = [&](auto jc) INLINE {
-          constexpr int j = decltype(jc)::value;
-          if constexpr (j >= 2 && j < 2 + 2 * KC_PER_T && (j - 2) % 2 == 0) store_k(ip, sk, (j - 2) / 2);
-          if constexpr (j == 2 + 2 * KC_PER_T) load_k(kt_k, sk);
-        };
-        auto softmax_v = [&](int kt_s) INLINE {
-#pragma unroll
-          for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
-          load_v(kt_v, sv);
-          softmax(kt_s);
-        };
-        if (A) stream(YES, YES, ip, 1 - ip, stage_hook);
-        else softmax_v(kt[0]);
-        __syncthreads();
-        if (!A) {
-          stream(YES, YES, ip, 1 - ip, stage_hook);
-        } else {
-#pragma unroll
-          for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
-          load_v(kt_v, sv);
-          if (it + 1 < n_tiles) softmax(kt[1]);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
-        kt[4] = tile_or_none(it + 5);
-        __syncthreads();
-      };
-      const std::integral_constant<int, 0> P0;
-      const std::integral_constant<int, 1> P1;
-      for (; it + 1 < n_tiles; it += 2) {
-        iteration(P0);
-        ++it;
-        iteration(P1);
-        --it;
-      }
-      if (it < n_tiles) iteration(P0);
-    };
-    if (__builtin_amdgcn_readfirstlane(wave) < 4) run(YES);
-    else run(NO);
-  }
-
-  if (t >= n_q) return;
-  const float inv = (l_run > 0.f) ? 1.f / l_run : 0.f;
-  bf16_t* op = a.o + o_off + (int64_t)p * a.o_sh + (int64_t)t * a.o_st + 4 * g;
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    uint2 u;
-    u.x = pack_bf16x2(acc[cb][0] * inv, acc[cb][1] * inv);
-    u.y = pack_bf16x2(acc[cb][2] * inv, acc[cb][3] * inv);
-    *reinterpret_cast<uint2*>(op + 16 * cb) = u;
-  }
-  if (a.lse && g == 0) {
-    float v = (l_run > 0.f) ? m_run * a.scale + logf(l_run) : -INFINITY;
-    a.lse[lse_off + (int64_t)p * n_q + t] = v;
-  }
-}
-
-// ---- head dim 256, GQA other than 2: 16-query waves ----
 // A work item holds QB 16-query blocks (q16_blocks) of one q-tile for all m
-// heads of the GQA group: wave w owns head w / QB and block w % QB, on
-// v_mfma_f32_16x16x32_bf16.  With 32-query waves these shapes need one wave
-// per SIMD at 512 VGPRs (and spill at m = 1 and m > 2); 16-query waves halve
-// O, Q and S per wave.  All waves run the same phase, one barrier per tile.
+// heads of the GQA group: wave w owns head w / QB and block w % QB.  With
+// 32-query waves these shapes need one wave per SIMD at 512 VGPRs (and spill
+// at m = 1 and m > 2); 16-query waves halve O, Q and S per wave.  K and V
+// live in separate two-slot rings offset by one tile (three combined stages
+// of 256 channels, 212 KiB, would not fit the LDS; the rings take 141 KiB).
+//
+// GQA 2 (eight waves): the ping-pong, group A = head 0 (waves 0-3), group
+// B = head 1 (waves 4-7), one wave of each per SIMD.  In the phases of
+// iteration i the streams read K(i+1) and V(i), while K(i+2) and V(i+1) are
+// staged into the other slots.
+// Other group sizes: all waves run the same phase, one barrier per tile.
 // Iteration i streams PV(i - 1) and QK(i) and takes the softmax of tile i;
-// K and V sit in two-slot rings offset by one tile, and between the MFMAs
-// each thread stores its chunks of K(i + 1) and V(i) and then fetches those
-// of K(i + 2) and V(i + 1).
+// between the MFMAs each thread stores its chunks of K(i + 1) and V(i) and
+// then fetches those of K(i + 2) and V(i + 1).
 template <int C, int M, bool DENSE, bool PAGED>
 __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(PrefillArgs a) {
   constexpr int QB = q16_blocks(M), PARTS = 4 / QB;
   constexpr int NW = M * QB, NT = 64 * NW;
+  // GQA 2: ping-pong between the two heads' waves (one of each per SIMD)
+  constexpr bool PP = M == 2;
   constexpr int KROW = C + 8, VROW = TILE + 8;
   constexpr int K_SLOT = TILE * KROW, V_SLOT = C * VROW;
   constexpr int K_CHUNKS = TILE * C / 8, V_UNITS = (TILE / 2) * (C / 8);
@@ -1205,12 +893,12 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   struct KSet { uint4 k[KC_PER_T]; };
   struct VSet { uint4 v[VU_PER_T][2]; };
   auto locate = [&](int kt) INLINE -> TileAt { return kvt.locate(kt); };
-  auto load_k = [&](const TileAt& at, KSet& sk) INLINE {
+  auto load_k_at = [&](const TileAt& at, KSet& sk) INLINE {
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
       if (k_mine(i)) sk.k[i] = bload16(krs, kvt.off(at, k_row[i], k_ce[i], k_boff[i]));
   };
-  auto load_v = [&](const TileAt& at, VSet& sv) INLINE {
+  auto load_v_at = [&](const TileAt& at, VSet& sv) INLINE {
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (v_mine(i)) {
@@ -1218,6 +906,10 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
         sv.v[i][1] = bload16(vrs, kvt.off(at, 2 * v_j[i] + 1, v_ce[i], v_boff[i] + st_bytes));
       }
   };
+  // the ping-pong reads a tile's page numbers where its fetch is issued
+  // (taking them out of the streams keeps 8 more VGPRs live, which spill)
+  auto load_k = [&](int kt, KSet& sk) INLINE { load_k_at(kvt.locate(kt), sk); };
+  auto load_v = [&](int kt, VSet& sv) INLINE { load_v_at(kvt.locate(kt), sv); };
   bf16_t* const kring = lds;                  // [2][K_SLOT]
   bf16_t* const vring = lds + 2 * K_SLOT;     // [2][V_SLOT]
   auto store_k = [&](int slot, const KSet& sk, int i) INLINE {
@@ -1292,6 +984,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   };
   const std::true_type YES;
   const std::false_type NO;
+  auto no_hook = [](auto) INLINE {};
 
   auto exp_pack = [&](float moff) INLINE -> float {
     float r0 = 0.f, r1 = 0.f;
@@ -1353,67 +1046,146 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
     l_run += rs;
   };
 
-  if (n_tiles > 0) {
-    // entering iteration i: K(i) is in K slot i & 1 and V(i - 1) in V slot
-    // (i - 1) & 1; sk holds K(i + 1), sv holds V(i); kt[j] is tile i + j,
-    // at1 / at2 locate tiles i + 1 / i + 2
-    KSet sk;
-    VSet sv;
-    int kt[3];
-#pragma unroll
-    for (int j = 0; j < 3; ++j) kt[j] = tile_or_none(j);
-    TileAt at1 = locate(kt[0]);
-    load_k(at1, sk);
-#pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
-    load_v(at1, sv);
-    at1 = locate(kt[1]);
-    TileAt at2 = locate(kt[2]);
-    load_k(at1, sk);
-    __syncthreads();
-    constexpr int L0 = 2 + 2 * (KC_PER_T + VU_PER_T);
-    static_assert(L0 < 4 * NKC, "staging must fit between the QK MFMAs");
-    // iteration i (parity ip): PV(i - 1) from V slot 1 - ip and QK(i) from
-    // K slot ip; K(i + 1) goes into K slot 1 - ip and V(i) into V slot ip
-    auto iteration = [&](auto ipc, auto pv, auto qk, int i) INLINE {
-      constexpr int ip = decltype(ipc)::value;
-      constexpr bool QK = decltype(qk)::value;
-      auto stage_hook = [&](auto jc) INLINE {
-        constexpr int j = decltype(jc)::value;
-        if constexpr (QK) {
-          if constexpr (j >= 2 && j < 2 + 2 * KC_PER_T && j % 2 == 0) store_k(1 - ip, sk, (j - 2) / 2);
-          if constexpr (j >= 2 + 2 * KC_PER_T && j < L0 && j % 2 == 0)
-            store_v(ip, sv, (j - 2 - 2 * KC_PER_T) / 2);
-          if constexpr (j == L0) {
-            load_k(at2, sk);
-            load_v(at1, sv);
+  if constexpr (PP) {
+    if (n_tiles > 0) {
+      // sk holds the K part of tile i + 2, sv the V part of tile i + 1
+      KSet sk;
+      VSet sv;
+      int kt[5];   // tiles i .. i + 4
+  #pragma unroll
+      for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
+      load_k(kt[0], sk);
+      load_v(kt[0], sv);
+  #pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
+  #pragma unroll
+      for (int i = 0; i < VU_PER_T; ++i) store_v(0, sv, i);
+      load_k(kt[1], sk);
+  #pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i) store_k(1, sk, i);
+      load_k(kt[2], sk);
+      load_v(kt[1], sv);
+      __syncthreads();
+      auto run = [&](auto is_a) INLINE {
+        constexpr bool A = decltype(is_a)::value;
+        if (A) stream(NO, YES, 0, 0, no_hook);
+        __syncthreads();
+        if (A) softmax(kt[0]);
+        else stream(NO, YES, 0, 0, no_hook);
+        __syncthreads();
+        int it = 0;
+        // iteration i (tile parity ip = i & 1): phases Y_i, X_i+1.  The streams
+        // read V(i) (V slot ip) and K(i+1) (K slot 1 - ip); each thread stages
+        // its K chunks of tile i + 2 into K slot ip between the MFMAs of its
+        // stream and then fetches those of tile i + 3, and in its softmax phase
+        // stores its V units of tile i + 1 into V slot 1 - ip and fetches those
+        // of tile i + 2.
+        auto iteration = [&](auto ipc) INLINE {
+          constexpr int ip = decltype(ipc)::value;
+          const int kt_k = kt[3], kt_v = kt[2];
+          auto stage_hook = [&](auto jc) INLINE {
+            constexpr int j = decltype(jc)::value;
+            if constexpr (j >= 2 && j < 2 + 2 * KC_PER_T && (j - 2) % 2 == 0) store_k(ip, sk, (j - 2) / 2);
+            if constexpr (j == 2 + 2 * KC_PER_T) load_k(kt_k, sk);
+          };
+          auto softmax_v = [&](int kt_s) INLINE {
+  #pragma unroll
+            for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
+            load_v(kt_v, sv);
+            softmax(kt_s);
+          };
+          if (A) stream(YES, YES, ip, 1 - ip, stage_hook);
+          else softmax_v(kt[0]);
+          __syncthreads();
+          if (!A) {
+            stream(YES, YES, ip, 1 - ip, stage_hook);
+          } else {
+  #pragma unroll
+            for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
+            load_v(kt_v, sv);
+            if (it + 1 < n_tiles) softmax(kt[1]);
           }
+  #pragma unroll
+          for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
+          kt[4] = tile_or_none(it + 5);
+          __syncthreads();
+        };
+        const std::integral_constant<int, 0> P0;
+        const std::integral_constant<int, 1> P1;
+        for (; it + 1 < n_tiles; it += 2) {
+          iteration(P0);
+          ++it;
+          iteration(P1);
+          --it;
+        }
+        if (it < n_tiles) iteration(P0);
+      };
+      if (__builtin_amdgcn_readfirstlane(wave) < 4) run(YES);
+      else run(NO);
+    }
+  } else {
+    if (n_tiles > 0) {
+      // entering iteration i: K(i) is in K slot i & 1 and V(i - 1) in V slot
+      // (i - 1) & 1; sk holds K(i + 1), sv holds V(i); kt[j] is tile i + j,
+      // at1 / at2 locate tiles i + 1 / i + 2
+      KSet sk;
+      VSet sv;
+      int kt[3];
+  #pragma unroll
+      for (int j = 0; j < 3; ++j) kt[j] = tile_or_none(j);
+      TileAt at1 = locate(kt[0]);
+      load_k_at(at1, sk);
+  #pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
+      load_v_at(at1, sv);
+      at1 = locate(kt[1]);
+      TileAt at2 = locate(kt[2]);
+      load_k_at(at1, sk);
+      __syncthreads();
+      constexpr int L0 = 2 + 2 * (KC_PER_T + VU_PER_T);
+      static_assert(L0 < 4 * NKC, "staging must fit between the QK MFMAs");
+      // iteration i (parity ip): PV(i - 1) from V slot 1 - ip and QK(i) from
+      // K slot ip; K(i + 1) goes into K slot 1 - ip and V(i) into V slot ip
+      auto iteration = [&](auto ipc, auto pv, auto qk, int i) INLINE {
+        constexpr int ip = decltype(ipc)::value;
+        constexpr bool QK = decltype(qk)::value;
+        auto stage_hook = [&](auto jc) INLINE {
+          constexpr int j = decltype(jc)::value;
+          if constexpr (QK) {
+            if constexpr (j >= 2 && j < 2 + 2 * KC_PER_T && j % 2 == 0) store_k(1 - ip, sk, (j - 2) / 2);
+            if constexpr (j >= 2 + 2 * KC_PER_T && j < L0 && j % 2 == 0)
+              store_v(ip, sv, (j - 2 - 2 * KC_PER_T) / 2);
+            if constexpr (j == L0) {
+              load_k_at(at2, sk);
+              load_v_at(at1, sv);
+            }
+          }
+        };
+        stream(pv, qk, 1 - ip, ip, stage_hook);
+        if constexpr (QK) {
+          softmax(kt[0]);
+          kt[0] = kt[1];
+          kt[1] = kt[2];
+          kt[2] = tile_or_none(i + 3);
+          at1 = at2;
+          at2 = locate(kt[2]);
+          __syncthreads();
         }
       };
-      stream(pv, qk, 1 - ip, ip, stage_hook);
-      if constexpr (QK) {
-        softmax(kt[0]);
-        kt[0] = kt[1];
-        kt[1] = kt[2];
-        kt[2] = tile_or_none(i + 3);
-        at1 = at2;
-        at2 = locate(kt[2]);
-        __syncthreads();
+      const std::integral_constant<int, 0> P0;
+      const std::integral_constant<int, 1> P1;
+      iteration(P0, NO, YES, 0);
+      int it = 1;
+      for (; it + 1 < n_tiles; it += 2) {
+        iteration(P1, YES, YES, it);
+        iteration(P0, YES, YES, it + 1);
       }
-    };
-    const std::integral_constant<int, 0> P0;
-    const std::integral_constant<int, 1> P1;
-    iteration(P0, NO, YES, 0);
-    int it = 1;
-    for (; it + 1 < n_tiles; it += 2) {
-      iteration(P1, YES, YES, it);
-      iteration(P0, YES, YES, it + 1);
-    }
-    if (it < n_tiles) {
-      iteration(P1, YES, YES, it);
-      iteration(P0, YES, NO, it + 1);
-    } else {
-      iteration(P1, YES, NO, it);
+      if (it < n_tiles) {
+        iteration(P1, YES, YES, it);
+        iteration(P0, YES, NO, it + 1);
+      } else {
+        iteration(P1, YES, NO, it);
+      }
     }
   }
 
@@ -1470,26 +1242,14 @@ hipError_t launch_q16(const PrefillArgs& a, int n_work, hipStream_t s) {
   return launch_kernel<prefill_q16_kernel<C, M, DENSE, PAGED>>(a, n_work, 64 * M * q16_blocks(M), lds, s);
 }
 
-template <bool DENSE, bool PAGED>
-hipError_t launch_wide(const PrefillArgs& a, int n_work, hipStream_t s) {
-  constexpr int lds = (2 * TILE * 264 + 2 * 256 * (TILE + 8)) * 2;
-  static_assert(lds <= 160 * 1024, "LDS budget");
-  return launch_kernel<prefill_wide_kernel<DENSE, PAGED>>(a, n_work, 512, lds, s);
-}
-
 template <int C, int M>
 hipError_t launch_c_m(const PrefillArgs& a, bool dense, int n_work, hipStream_t s) {
   const bool paged = a.kv.paged != 0;
   if constexpr (C == 256) {
-    if constexpr (M == 2) {   // the 16-query ping-pong
-      if (dense) return paged ? launch_wide<true, true>(a, n_work, s) : launch_wide<true, false>(a, n_work, s);
-      return paged ? launch_wide<false, true>(a, n_work, s) : launch_wide<false, false>(a, n_work, s);
-    } else {
-      if (dense) return paged ? launch_q16<C, M, true, true>(a, n_work, s)
-                              : launch_q16<C, M, true, false>(a, n_work, s);
-      return paged ? launch_q16<C, M, false, true>(a, n_work, s)
-                   : launch_q16<C, M, false, false>(a, n_work, s);
-    }
+    if (dense) return paged ? launch_q16<C, M, true, true>(a, n_work, s)
+                            : launch_q16<C, M, true, false>(a, n_work, s);
+    return paged ? launch_q16<C, M, false, true>(a, n_work, s)
+                 : launch_q16<C, M, false, false>(a, n_work, s);
   } else {
     if (dense) return paged ? launch_one<C, M, true, true>(a, n_work, s)
                             : launch_one<C, M, true, false>(a, n_work, s);
