@@ -103,7 +103,8 @@ enum { BFLA_KV_CONTIGUOUS = 0, BFLA_KV_PAGED = 1 };
  *             at  base + P*page_stride + (t % page_size)*stride_tok +
  *             h*stride_head + c.  The pool holds n_pages pages and must be
  *             smaller than 2 GiB; a table entry outside [0, n_pages) reads as
- *             zeros (never out of bounds). */
+ *             zeros (never out of bounds).  head_dim <= stride_tok < 2^24
+ *             (BFLA_ERR_INVALID_ARG below, BFLA_ERR_UNSUPPORTED above). */
 typedef struct bfla_kv {
   int32_t layout;               /* BFLA_KV_CONTIGUOUS or BFLA_KV_PAGED */
   const void* k;                /* device, bf16 */

@@ -164,6 +164,14 @@ int check_kv(const bfla_problem* prob, const bfla_kv* kv, bool need_v) {
     if (!kv->block_table) return fail(BFLA_ERR_INVALID_ARG, "block_table is NULL");
     if (kv->page_stride % 8 || kv->page_stride < 1)
       return fail(BFLA_ERR_INVALID_ARG, "page_stride must be a positive multiple of 8");
+    // the prefill addresses a 64-token tile as if contiguous and maps it onto
+    // its pages: token rows must not overlap and a tile must span < 2 GiB
+    if (kv->stride_tok < prob->head_dim)
+      return fail(BFLA_ERR_INVALID_ARG, "paged stride_tok %lld < head_dim %d",
+                  (long long)kv->stride_tok, prob->head_dim);
+    if (kv->stride_tok >= (int64_t(1) << 24))
+      return fail(BFLA_ERR_UNSUPPORTED, "paged stride_tok %lld >= 2^24",
+                  (long long)kv->stride_tok);
     for (int r = 0; r < prob->batch; ++r)
       if (cdiv(prob->n_kv[r], kv->page_size) > kv->max_pages)
         return fail(BFLA_ERR_INVALID_ARG, "request %d needs %lld pages > max_pages %d", r,

@@ -313,14 +313,25 @@ prefill_kernel(PrefillArgs a) {
     uint4 v[VU_PER_T][2];
   };
 
-  // Byte offset of (key, 8-channel chunk ce) in a paged pool, given the page
-  // numbers of the tile's (up to 4) pages read as scalars.
-  auto paged_off = [&](int tok0, int kr, int ce, const int* pg) INLINE -> uint32_t {
-    const int key = tok0 + kr;
-    if (key >= n_kv) return 0x80000000u;
-    const int slot = ps >= TILE ? 0 : (kr >> ps_shift);
-    const int page = slot == 0 ? pg[0] : slot == 1 ? pg[1] : slot == 2 ? pg[2] : pg[3];
-    return (uint32_t)page * page_bytes + (uint32_t)(((key & (ps - 1)) * st + 8 * ce) * 2);
+  // Paged offsets from the chunk's offset inside a contiguous tile, boff =
+  // (kr * st + 8 ce) * 2 for key kr of the tile: the page slot of the chunk
+  // is the number of thresholds j * ps * st * 2 that boff reaches, and its
+  // byte offset is boff + base[slot], with base[j] = pg[j] * page_bytes +
+  // (tok0 % ps) * st * 2 - j * ps * st * 2 read per tile as scalars.  Keys
+  // past N_kv (boff >= (N_kv - tok0) * st * 2, as 8 ce + 8 <= C <= st) and bad
+  // pages give offsets >= 2^31, past the pool's range.
+  struct PagedTile {
+    uint32_t base[4];
+    uint32_t lim;
+  };
+  const uint32_t slot_bytes = ps < TILE ? (uint32_t)(ps * st * 2) : 0xFFFFFFFFu;
+  const uint32_t thr2 = ps < TILE / 2 ? 2 * slot_bytes : 0xFFFFFFFFu;
+  const uint32_t thr3 = ps < TILE / 2 ? 3 * slot_bytes : 0xFFFFFFFFu;
+  auto paged_off = [&](const PagedTile& pt, uint32_t boff) INLINE -> uint32_t {
+    if (boff >= pt.lim) return 0x80000000u;
+    const uint32_t b = boff < slot_bytes ? pt.base[0] : boff < thr2 ? pt.base[1]
+                     : boff < thr3 ? pt.base[2] : pt.base[3];
+    return b + boff;
   };
 
   // Fetch this thread's K chunks (part & 1) and/or V units (part & 2) of
@@ -344,25 +355,29 @@ prefill_kernel(PrefillArgs a) {
         }
       return;
     }
-    // paged: the tile's page numbers (a bad tile reads page -1 -> zeros)
+    // paged: the tile's page bases (a bad tile or table entry reads zeros)
     const int tok0 = ok ? kt * TILE : 0;
-    int pg[4];
+    PagedTile pt;
+    pt.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
+    const uint32_t in_page = (uint32_t)((tok0 & (ps - 1)) * st * 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int tk = tok0 + (j << ps_shift);
       const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
-      pg[j] = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
-      if ((unsigned)pg[j] >= (unsigned)a.kv.n_pages) pg[j] = -1;  // entry outside the pool
+      const int pg = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
+      pt.base[j] = (unsigned)pg < (unsigned)a.kv.n_pages
+                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)(ps * st * 2)
+                       : 0x80000000u;
     }
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
       if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
-        sg.k[i] = bload16(krs, paged_off(tok0, k_row[i], k_ce[i], pg));
+        sg.k[i] = bload16(krs, paged_off(pt, k_boff[i]));
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (LV && (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS)) {
-        sg.v[i][0] = bload16(vrs, paged_off(tok0, 2 * v_j[i], v_ce[i], pg));
-        sg.v[i][1] = bload16(vrs, paged_off(tok0, 2 * v_j[i] + 1, v_ce[i], pg));
+        sg.v[i][0] = bload16(vrs, paged_off(pt, v_boff[i]));
+        sg.v[i][1] = bload16(vrs, paged_off(pt, v_boff[i] + st_bytes));
       }
   };
   const std::integral_constant<int, 1> K_PART;

@@ -150,8 +150,22 @@ def test_entry_points_reject_before_launch():
     st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
                               None, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
-    # pool of 2 GiB or more
+    # token rows narrower than a head (overlapping), or a 64-token tile of 2 GiB
     pk.page_size = 16
+    pk.stride_tok = 32
+    st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
+                              None, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
+    pk.stride_tok = 1 << 24
+    pk.page_stride = 16 << 24
+    pk.n_pages = 1  # a pool of one page stays under 2 GiB
+    st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
+                              None, None)
+    assert st == bfla.BFLA_ERR_UNSUPPORTED
+    assert b"2^24" in L.bfla_last_error()
+    pk.stride_tok = 128
+    pk.page_stride = 16 * 128
+    # pool of 2 GiB or more
     pk.n_pages = 1 << 20
     st = L.bfla_dense_prefill(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(pk), C.byref(v),
                               None, None)
