@@ -710,14 +710,17 @@ prefill_kernel(PrefillArgs a) {
   }
 }
 
-// Where the keys of KV tile kt are, for the 16-query kernels.  Contiguous:
-// the tile's first byte in the head's rows.  Paged: its first key and the
-// numbers of the (up to four) pages it spans, read as scalars; tiles outside
-// [0, T_kv), keys past N_kv and table entries outside the pool give offsets
-// past the descriptor's range, which read zeros.
+// Where the keys of KV tile kt are, for the 16-query kernels, given a chunk's
+// byte offset inside a contiguous tile, boff = (kr * st + 8 ce) * 2 for key
+// kr of the tile.  Contiguous: the tile's first byte plus boff.  Paged, as in
+// prefill_kernel: per tile, scalar bases pg[j] * page_bytes + (tok0 % ps) *
+// st * 2 - j * ps * st * 2 of its (up to four) pages, a chunk taking the base
+// of the slot whose threshold j * ps * st * 2 its boff reaches.  Tiles
+// outside [0, T_kv), keys past N_kv and table entries outside the pool give
+// offsets past the descriptor's range, which read zeros.
 struct TileAt {
-  uint32_t base;
-  int pg[4];
+  uint32_t base[4];
+  uint32_t lim;   // paged: boff of the first key past N_kv (or past the tile)
 };
 template <bool PAGED>
 struct KvTiles {
@@ -725,38 +728,36 @@ struct KvTiles {
   uint32_t tile_bytes;     // contiguous: bytes per 64-key tile
   const int32_t* bt;       // paged: this request's block-table row
   int ps_shift, n_pages;
-  uint32_t page_bytes;
+  uint32_t page_bytes, slot_bytes, thr2, thr3;
   int64_t st;              // elements per token
 
   __device__ __forceinline__ TileAt locate(int kt) const {
     TileAt at;
     const bool ok = (unsigned)kt < (unsigned)t_kv;
     if (!PAGED) {
-      at.base = ok ? (uint32_t)kt * tile_bytes : 0x80000000u;
+      at.base[0] = ok ? (uint32_t)kt * tile_bytes : 0x80000000u;
       return at;
     }
     const int tok0 = ok ? kt * TILE : 0;
+    at.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
+    const uint32_t in_page = (uint32_t)((tok0 & ((1 << ps_shift) - 1)) * st * 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int tk = tok0 + (j << ps_shift);
       const bool used = j == 0 || (j << ps_shift) < TILE;
-      const int pgj = (ok && used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
-      at.pg[j] = (unsigned)pgj >= (unsigned)n_pages ? -1 : pgj;
+      const int pg = (ok && used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
+      at.base[j] = (unsigned)pg < (unsigned)n_pages
+                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)((st * 2) << ps_shift)
+                       : 0x80000000u;
     }
-    at.base = ok ? (uint32_t)tok0 : 0x80000000u;
     return at;
   }
-  // byte offset of (key kr of the tile, 8-channel chunk ce); `contig` is
-  // that offset inside a contiguous tile
-  __device__ __forceinline__ uint32_t off(const TileAt& at, int kr, int ce, uint32_t contig) const {
-    if (!PAGED) return at.base + contig;
-    if (at.base == 0x80000000u) return 0x80000000u;
-    const int key = (int)at.base + kr;
-    if (key >= n_kv) return 0x80000000u;
-    const int slot = (1 << ps_shift) >= TILE ? 0 : (kr >> ps_shift);
-    const int page = slot == 0 ? at.pg[0] : slot == 1 ? at.pg[1] : slot == 2 ? at.pg[2] : at.pg[3];
-    return (uint32_t)page * page_bytes +
-           (uint32_t)(((key & ((1 << ps_shift) - 1)) * st + 8 * ce) * 2);
+  __device__ __forceinline__ uint32_t off(const TileAt& at, uint32_t boff) const {
+    if (!PAGED) return at.base[0] + boff;
+    if (boff >= at.lim) return 0x80000000u;
+    const uint32_t b = boff < slot_bytes ? at.base[0] : boff < thr2 ? at.base[1]
+                     : boff < thr3 ? at.base[2] : at.base[3];
+    return b + boff;
   }
 };
 template <int C, bool PAGED>
@@ -776,7 +777,7 @@ __device__ __forceinline__ KvTiles<PAGED> kv_tiles(const PrefillArgs& a, const R
     kt.bt = nullptr;
     kt.ps_shift = 0;
     kt.n_pages = 0;
-    kt.page_bytes = 0;
+    kt.page_bytes = kt.slot_bytes = kt.thr2 = kt.thr3 = 0;
   } else {
     const int64_t head_off = (int64_t)h * a.kv.stride_head;
     krs = make_rsrc(a.kv.k + head_off, a.kv.pool_bytes);
@@ -785,6 +786,10 @@ __device__ __forceinline__ KvTiles<PAGED> kv_tiles(const PrefillArgs& a, const R
     kt.ps_shift = __builtin_ctz(a.kv.page_size);   // power of two >= 16
     kt.n_pages = a.kv.n_pages;
     kt.page_bytes = (uint32_t)(a.kv.page_stride * 2);
+    const int ps = a.kv.page_size;
+    kt.slot_bytes = ps < TILE ? (uint32_t)(ps * kt.st * 2) : 0xFFFFFFFFu;
+    kt.thr2 = ps < TILE / 2 ? 2 * kt.slot_bytes : 0xFFFFFFFFu;
+    kt.thr3 = ps < TILE / 2 ? 3 * kt.slot_bytes : 0xFFFFFFFFu;
   }
   return kt;
 }
@@ -911,14 +916,14 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   auto load_k_at = [&](const TileAt& at, KSet& sk) INLINE {
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
-      if (k_mine(i)) sk.k[i] = bload16(krs, kvt.off(at, k_row[i], k_ce[i], k_boff[i]));
+      if (k_mine(i)) sk.k[i] = bload16(krs, kvt.off(at, k_boff[i]));
   };
   auto load_v_at = [&](const TileAt& at, VSet& sv) INLINE {
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (v_mine(i)) {
-        sv.v[i][0] = bload16(vrs, kvt.off(at, 2 * v_j[i], v_ce[i], v_boff[i]));
-        sv.v[i][1] = bload16(vrs, kvt.off(at, 2 * v_j[i] + 1, v_ce[i], v_boff[i] + st_bytes));
+        sv.v[i][0] = bload16(vrs, kvt.off(at, v_boff[i]));
+        sv.v[i][1] = bload16(vrs, kvt.off(at, v_boff[i] + st_bytes));
       }
   };
   // the ping-pong reads a tile's page numbers where its fetch is issued
