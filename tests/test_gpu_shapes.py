@@ -69,12 +69,27 @@ def test_dense_shape(c, m):
 PAGED_CASES = [(256, m) for m in range(1, 9)] + [(128, 1), (128, 4), (128, 5), (64, 8)]
 
 
+# pages larger than a tile: a tile starts inside its page
+BIG_PAGE_CASES = [(128, 4, 128), (128, 4, 256), (128, 5, 256), (64, 1, 128), (256, 2, 256),
+                  (256, 3, 128), (256, 5, 256)]
+
+
 @pytest.mark.parametrize("c,m", PAGED_CASES, ids=[f"c{c}_m{m}" for c, m in PAGED_CASES])
 def test_paged_shape(c, m):
+    _paged_case(c, m, 16)
+
+
+@pytest.mark.parametrize("c,m,ps", BIG_PAGE_CASES,
+                         ids=[f"c{c}_m{m}_p{p}" for c, m, p in BIG_PAGE_CASES])
+def test_paged_shape_big_pages(c, m, ps):
+    _paged_case(c, m, ps)
+
+
+def _paged_case(c, m, page_size):
     """Sparse (oracle lists) and dense prefill on paged K/V, two KV heads."""
     wl = synth.workload("tiny_2k", h_q=2 * m, h_kv=2, head_dim=c, seed=200 + c + m)
     seqs = synth.make_inputs(wl, seqlens=[N])
-    pb = PagedBatch(seqs, [N], page_size=16, seed=7 + m)
+    pb = PagedBatch(seqs, [N], page_size=page_size, seed=7 + m)
     kw, prm = _params()
     s = seqs[0]
     q, k, v = s.q.double().numpy(), s.k.double().numpy(), s.v.double().numpy()
