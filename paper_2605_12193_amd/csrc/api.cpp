@@ -142,7 +142,7 @@ int check_kv(const bfla_problem* prob, const bfla_kv* kv, bool need_v) {
   if (kv->stride_head % 8 || kv->stride_tok % 8 || kv->stride_head < 1 || kv->stride_tok < 1)
     return fail(BFLA_ERR_INVALID_ARG, "kv strides must be positive multiples of 8");
   if (kv->layout == BFLA_KV_CONTIGUOUS) {
-    if (kv->stride_batch % 8) return fail(BFLA_ERR_INVALID_ARG, "kv stride_batch % 8 != 0");
+    if (kv->stride_batch % 8) return fail(BFLA_ERR_INVALID_ARG, "kv stride_batch %% 8 != 0");
     // one KV head of one request is read through a buffer descriptor whose
     // byte range is a signed 32-bit count
     for (int r = 0; r < prob->batch; ++r)
@@ -357,7 +357,7 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   for (int r = 0; r < prob->batch; ++r)
     if (cdiv(prob->n_kv[r], params->block) > kMaxBlocksPerRow)
       return fail(BFLA_ERR_UNSUPPORTED, "request %d: more than %d KV blocks", r,
-                  kMaxBlocksPerRow);
+                  (int)kMaxBlocksPerRow);
   Sizes s = sizes_of(prob, params);
   float* scores = dbg_scores;
   if (!scores) {

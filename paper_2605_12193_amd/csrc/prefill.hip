@@ -51,8 +51,8 @@ namespace {
 
 constexpr int TILE = 64;
 constexpr float LOG2E = 1.4426950408889634f;
-constexpr float RESCALE_LOG2 = 8.0f;
-constexpr float RESCALE_SUM = 256.0f;      // 2^RESCALE_LOG2
+constexpr int RESCALE_LOG2 = 8;
+constexpr float RESCALE_SUM = float(1 << RESCALE_LOG2);
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;  // raw buffer, 32-bit data format
 constexpr int VMCNT0 = 0x0F70;                // s_waitcnt vmcnt(0), other counters free
 
@@ -858,7 +858,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   const int ri = find_req(a.batch, w);
   const ReqDesc& Rd = a.batch.r[ri];
   const int n_q = Rd.n_q, n_kv = Rd.n_kv, t_q = Rd.t_q, t_kv = Rd.t_kv;
-  const int64_t q_off = Rd.q_off, o_off = Rd.o_off, kv_off = Rd.kv_off, lse_off = Rd.lse_off;
+  const int64_t q_off = Rd.q_off, o_off = Rd.o_off, lse_off = Rd.lse_off;
   const int local = w - Rd.work_begin;
   const int h = local % a.h_kv;
   const int rank = local / a.h_kv;
