@@ -926,8 +926,6 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
         sv.v[i][1] = bload16(vrs, kvt.off(at, v_boff[i] + st_bytes));
       }
   };
-  // the ping-pong reads a tile's page numbers where its fetch is issued
-  // (taking them out of the streams keeps 8 more VGPRs live, which spill)
   auto load_k = [&](int kt, KSet& sk) INLINE { load_k_at(kvt.locate(kt), sk); };
   auto load_v = [&](int kt, VSet& sv) INLINE { load_v_at(kvt.locate(kt), sv); };
   bf16_t* const kring = lds;                  // [2][K_SLOT]
@@ -1085,6 +1083,9 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       for (int i = 0; i < KC_PER_T; ++i) store_k(1, sk, i);
       load_k(kt[2], sk);
       load_v(kt[1], sv);
+      // where the next fetches go, K of tile i + 3 and V of tile i + 2, read
+      // at the end of the previous iteration (paged: outside the MFMA streams)
+      TileAt at_k = locate(kt[3]), at_v = locate(kt[2]);
       __syncthreads();
       auto run = [&](auto is_a) INLINE {
         constexpr bool A = decltype(is_a)::value;
@@ -1102,16 +1103,15 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
         // of tile i + 2.
         auto iteration = [&](auto ipc) INLINE {
           constexpr int ip = decltype(ipc)::value;
-          const int kt_k = kt[3], kt_v = kt[2];
           auto stage_hook = [&](auto jc) INLINE {
             constexpr int j = decltype(jc)::value;
             if constexpr (j >= 2 && j < 2 + 2 * KC_PER_T && (j - 2) % 2 == 0) store_k(ip, sk, (j - 2) / 2);
-            if constexpr (j == 2 + 2 * KC_PER_T) load_k(kt_k, sk);
+            if constexpr (j == 2 + 2 * KC_PER_T) load_k_at(at_k, sk);
           };
           auto softmax_v = [&](int kt_s) INLINE {
   #pragma unroll
             for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
-            load_v(kt_v, sv);
+            load_v_at(at_v, sv);
             softmax(kt_s);
           };
           if (A) stream(YES, YES, ip, 1 - ip, stage_hook);
@@ -1122,12 +1122,14 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
           } else {
   #pragma unroll
             for (int u = 0; u < VU_PER_T; ++u) store_v(1 - ip, sv, u);
-            load_v(kt_v, sv);
+            load_v_at(at_v, sv);
             if (it + 1 < n_tiles) softmax(kt[1]);
           }
   #pragma unroll
           for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
           kt[4] = tile_or_none(it + 5);
+          at_v = at_k;
+          at_k = locate(kt[3]);
           __syncthreads();
         };
         const std::integral_constant<int, 0> P0;
