@@ -334,9 +334,27 @@ prefill_kernel(PrefillArgs a) {
     return b + boff;
   };
 
+  // the page bases of tile kt (paged; read as scalars)
+  auto paged_tile = [&](int kt) INLINE -> PagedTile {
+    const bool ok = (unsigned)kt < (unsigned)t_kv;
+    const int tok0 = ok ? kt * TILE : 0;
+    PagedTile pt;
+    pt.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
+    const uint32_t in_page = (uint32_t)((tok0 & (ps - 1)) * st * 2);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tk = tok0 + (j << ps_shift);
+      const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
+      const int pg = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
+      pt.base[j] = (unsigned)pg < (unsigned)a.kv.n_pages
+                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)(ps * st * 2)
+                       : 0x80000000u;
+    }
+    return pt;
+  };
   // Fetch this thread's K chunks (part & 1) and/or V units (part & 2) of
   // tile kt into sg.
-  auto load_part = [&](int kt, Staged& sg, auto part) INLINE {
+  auto load_part_pt = [&](int kt, const PagedTile& pt, Staged& sg, auto part) INLINE {
     constexpr bool LK = (decltype(part)::value & 1) != 0, LV = (decltype(part)::value & 2) != 0;
     // tiles outside [0, T_kv) (malformed lists) load nothing
     const bool ok = (unsigned)kt < (unsigned)t_kv;
@@ -355,20 +373,6 @@ prefill_kernel(PrefillArgs a) {
         }
       return;
     }
-    // paged: the tile's page bases (a bad tile or table entry reads zeros)
-    const int tok0 = ok ? kt * TILE : 0;
-    PagedTile pt;
-    pt.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
-    const uint32_t in_page = (uint32_t)((tok0 & (ps - 1)) * st * 2);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tk = tok0 + (j << ps_shift);
-      const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
-      const int pg = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
-      pt.base[j] = (unsigned)pg < (unsigned)a.kv.n_pages
-                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)(ps * st * 2)
-                       : 0x80000000u;
-    }
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
       if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
@@ -379,6 +383,10 @@ prefill_kernel(PrefillArgs a) {
         sg.v[i][0] = bload16(vrs, paged_off(pt, v_boff[i]));
         sg.v[i][1] = bload16(vrs, paged_off(pt, v_boff[i] + st_bytes));
       }
+  };
+  auto load_part = [&](int kt, Staged& sg, auto part) INLINE {
+    if constexpr (PAGED) load_part_pt(kt, paged_tile(kt), sg, part);
+    else load_part_pt(kt, PagedTile{}, sg, part);
   };
   const std::integral_constant<int, 1> K_PART;
   const std::integral_constant<int, 2> V_PART;
@@ -589,6 +597,9 @@ prefill_kernel(PrefillArgs a) {
       store_tile(stage(1), sg1);
       load_tile(kt[2], sg0);
       load_tile(kt[3], sg1);
+      // the page bases of tile i + 4, read outside the MFMA streams
+      PagedTile pt4{};
+      if constexpr (PAGED) pt4 = paged_tile(kt[4]);
       __syncthreads();
       // Each group runs its own copy of the loop (same barriers in the same
       // order), so that the compiler sees one group's loads and stores as
@@ -618,12 +629,12 @@ prefill_kernel(PrefillArgs a) {
             constexpr int j = decltype(jc)::value;
             constexpr int K0 = 2, L0 = K0 + 2 * KC_PER_T;
             if constexpr (j >= K0 && j < L0 && (j - K0) % 2 == 0) store_k(dst, sg, (j - K0) / 2);
-            if constexpr (j == L0) load_part(kt_load, sg, K_PART);
+            if constexpr (j == L0) load_part_pt(kt_load, pt4, sg, K_PART);
           };
           auto softmax_v = [&](int kt_s) INLINE {
 #pragma unroll
             for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
-            load_part(kt_load, sg, V_PART);
+            load_part_pt(kt_load, pt4, sg, V_PART);
             softmax(kt_s);
           };
           // phase Y_i: A streams PV(i), QK(i+1); B takes the softmax of tile i
@@ -636,12 +647,13 @@ prefill_kernel(PrefillArgs a) {
           } else {
 #pragma unroll
             for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
-            load_part(kt_load, sg, V_PART);
+            load_part_pt(kt_load, pt4, sg, V_PART);
             if (it + 1 < n_tiles) softmax(kt[1]);
           }
 #pragma unroll
           for (int j = 0; j < 4; ++j) kt[j] = kt[j + 1];
           kt[4] = tile_or_none(it + 5);
+          if constexpr (PAGED) pt4 = paged_tile(kt[4]);
           slot = slot1;
           __syncthreads();
         };
