@@ -111,7 +111,8 @@ def test_block_probs_sum_to_one_and_match_library_softmax():
     np.testing.assert_allclose(a.astype(np.float64).sum(axis=1), 1.0, atol=2e-6)
     assert np.all(a[:, 30:] == 0)
     ref = torch.softmax(torch.from_numpy(s[:, :30].astype(np.float64)) * alpha, dim=1).numpy()
-    np.testing.assert_allclose(a[:, :30], ref, rtol=2e-5, atol=1e-7)
+    # float32 against float64: well inside the 1e-5 near-tie band (measured 3.2e-6)
+    np.testing.assert_allclose(a[:, :30], ref, rtol=4e-6, atol=1e-37)
     # adding a constant to a row leaves the probabilities unchanged
     a2 = O.block_probs(s + np.float32(64.0), alpha)
     np.testing.assert_allclose(a2, a, rtol=1e-5, atol=1e-7)
