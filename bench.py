@@ -6,14 +6,23 @@ sparse prefill.  Inputs are seeded synthetic bf16 tensors already resident in
 HBM.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload llama_128k|llama_32k|wide_64k|paged_4x|tiny_2k]
+                  [--only] [--no-cpu]
 
 `value` is the dense-equivalent throughput 4 * C * H_q * sum_r N_r (N_r + 1) / 2
 FLOP per step divided by the step time (the causal FlashAttention convention).
 The roofline object reports the sparse prefill kernel (the dominant one):
 4 * T^2 * C * m FLOP per kept (KV head, q-tile, kv-tile) tile over its average
 launch time from HIP events on the launch stream, against the bf16 dense MFMA
-peak.  cpu_baseline is the CPU oracle timed on a bounded random sample of
-(request, KV head, q-tile) rows of the same workload.
+peak.
+
+The default run (the 128K Llama-shaped layer) also carries, unless --only:
+* `sweep_128k`: the same layer at gamma in {0.8, 0.9, 0.95} x rho in {0, 0.1}
+  (keep ratio, stage times, speedup over dense, kept-tile fraction);
+* `llama_32k`: the 32K layer with its own stage times, dense time, speedup
+  and rooflines.
+`cpu_baseline` is the CPU oracle on the same workload: Stage 1 and the tile
+stage in full, the sparse attention on a stratified sample of (request, KV
+head, q-tile) rows, extrapolated to every row by kept-tile count.
 """
 from __future__ import annotations
 
@@ -53,9 +62,13 @@ def parse():
     ap.add_argument("--n-local", type=int, default=None)
     ap.add_argument("--eta", type=int, default=None)
     ap.add_argument("--dense-steps", type=int, default=3)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="time budget of the oracle sample")
-    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sweep-steps", type=int, default=5,
+                    help="timed passes per point of the 128K threshold sweep")
+    ap.add_argument("--cpu-rows", type=int, default=256,
+                    help="(request, KV head, q-tile) rows of the oracle's attention sample")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle leg")
+    ap.add_argument("--only", action="store_true",
+                    help="time the named workload only (no threshold sweep, no 32K record)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this many MiB once (a dispatch "
                          "of known HBM traffic for scaling FETCH_SIZE / WRITE_SIZE)")
@@ -169,85 +182,370 @@ class Inputs:
         return o[a + t0:a + t1, p].float().cpu().numpy()
 
 
-def cpu_baseline(wl, inp, gpu_o, budget_s, gpu_mask=None, seed=0):
-    """Time the oracle on random (request, KV head, q-tile) rows: Stage 1 of
-    the query block holding the q-tile (all m query heads of the KV head), the
-    tile stage of that block row, and the sparse attention of the q-tile.
-    Also returns the GPU-vs-oracle error on the sampled outputs and, given the
-    GPU block mask (host uint8, the library's packed layout), its agreement
-    with the oracle's mask on the sampled block rows: every sure cell must
-    match; near-tie cells are counted, and so are the ones that differ."""
-    from oracle import bfla_oracle as O
+
+
+def cpu_info():
+    """Threads the oracle's library matmuls use, the cores this process may
+    run on, and the host CPU model."""
     try:
         from threadpoolctl import threadpool_info
-        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+        blas = [d for d in threadpool_info() if d.get("user_api") == "blas"]
+        threads = max([d.get("num_threads", 1) for d in blas] + [1])
     except Exception:
-        cores = os.cpu_count() or 1
+        threads = os.cpu_count() or 1
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return int(threads), int(nproc), model
+
+
+def stratified_rows(n_tokens, h_kv, tile, want, rng):
+    """At least `want` (request, KV head, q-tile) rows: every (request, KV
+    head) gets the same number of q-tile strata (equal ranges of q-tiles) and
+    one uniformly drawn q-tile from each."""
+    pairs = [(r, h) for r in range(len(n_tokens)) for h in range(h_kv)]
+    per = -(-want // len(pairs))
+    rows = []
+    for r, h in pairs:
+        t_q = -(-n_tokens[r] // tile)
+        edges = np.linspace(0, t_q, min(per, t_q) + 1).astype(int)
+        for a, b in zip(edges[:-1], edges[1:]):
+            if b > a:
+                rows.append((r, h, int(rng.integers(a, b))))
+    return rows
+
+
+def cpu_baseline(wl, inp, gpu_o, gpu_mask, gpu_rp, gpu_cols, rows=256, seed=0):
+    """The CPU oracle on the same workload, on this host.
+
+    Stage 1 (block scores, keep-mass selection, GQA union) and the tile stage
+    (expansion, band, sink, rescue, lists) run in full; the sparse attention
+    runs on a stratified sample of (request, KV head, q-tile) rows over the
+    oracle's own lists, and its time is extrapolated to every row by the
+    ratio of all kept tiles to the sample's kept tiles.  Also returns the GPU
+    block mask against the oracle's on every cell (sure cells must match;
+    near-tie cells are counted), the rows whose GPU list differs from the
+    oracle's, and the GPU outputs on the sampled rows against the oracle's
+    attention over the GPU's own lists."""
+    from oracle import bfla_oracle as O
+    threads, nproc, model = cpu_info()
     T, b = wl.tile, wl.block
     m = wl.h_q // wl.h_kv
     alpha = O.default_scale(wl.head_dim)
-    rng = np.random.default_rng(seed)
-    rows = [(r, qt) for r, n in enumerate(inp.n) for qt in range(-(-n // T))]
-    order = rng.permutation(len(rows))
-    heads = rng.integers(0, wl.h_kv, len(rows))
-    host = {}
-    L = [-(-n // b) for n in inp.n]
-    mask_off = np.concatenate([[0], np.cumsum([wl.h_kv * x * x for x in L])]).astype(np.int64)
-    mchk = {"block_rows": 0, "blocks": 0, "sure_mismatch": 0, "tie_blocks": 0, "tie_mismatch": 0}
-    seen = set()
-    flop = 0.0
+    t_stage1 = t_expand = 0.0
+    mchk = {"cells": 0, "sure_mismatch": 0, "tie_cells": 0, "tie_mismatch": 0}
+    list_rows = list_rows_differ = 0
+    host, lists, row_base = [], [], []
+    mask_off = base = kept_total = 0
+    for r, s in enumerate(inp.seqs):
+        n = inp.n[r]
+        # bf16 -> float64 inputs (data marshalling, not timed)
+        q, k, v = (t.double().numpy() for t in (s.q, s.k, s.v))
+        t0 = time.perf_counter()
+        st = O.estimate_mask(q, k, b, wl.group, wl.gamma, alpha)
+        t_stage1 += time.perf_counter() - t0
+        L = st["mask"].shape[1]
+        g = gpu_mask[mask_off:mask_off + wl.h_kv * L * L].reshape(st["mask"].shape)
+        mask_off += wl.h_kv * L * L
+        tie = st["status"] == O.TIE
+        diff = g != st["mask"]
+        mchk["cells"] += int(g.size)
+        mchk["sure_mismatch"] += int(np.sum(diff & ~tie))
+        mchk["tie_cells"] += int(np.sum(tie))
+        mchk["tie_mismatch"] += int(np.sum(diff & tie))
+        t0 = time.perf_counter()
+        orp, ocols, _ = O.expand_rescue([st["mask"]], [n], [n], b, T, wl.n_local, wl.n_sink,
+                                        wl.eta, wl.rho, wl.seed)
+        t_expand += time.perf_counter() - t0
+        n_rows = len(orp) - 1
+        g_counts = np.diff(gpu_rp[base:base + n_rows + 1])
+        o_counts = np.diff(orp)
+        same = g_counts == o_counts
+        for i in np.flatnonzero(same):
+            a = gpu_rp[base + i]
+            if not np.array_equal(gpu_cols[a:a + g_counts[i]], ocols[orp[i]:orp[i + 1]]):
+                same[i] = False
+        list_rows += n_rows
+        list_rows_differ += int(np.sum(~same))
+        kept_total += int(orp[-1])
+        host.append((q, k, v))
+        lists.append((orp, ocols))
+        row_base.append(base)
+        base += n_rows
+        del st
+    sample = stratified_rows(inp.n, wl.h_kv, T, rows, np.random.default_rng(seed))
+    t_attn = 0.0
+    kept_sample = 0
     max_abs, num, den = 0.0, 0.0, 0.0
-    t0 = time.perf_counter()
-    done = 0
-    for idx in order:
-        if time.perf_counter() - t0 >= budget_s:
-            break
-        r, qt = rows[idx]
-        h = int(heads[idx])
-        if r not in host:
-            s = inp.seqs[r]
-            host[r] = tuple(x.float().numpy() for x in (s.q, s.k, s.v))
+    for r, h, qt in sample:
         q, k, v = host[r]
-        n = q.shape[1]
-        done += 1
-        i = qt // (b // T)
-        st = O.estimate_mask(q[h * m:(h + 1) * m, i * b:(i + 1) * b].astype(np.float64),
-                             k[h:h + 1, :min(n, (i + 1) * b)].astype(np.float64), b,
-                             wl.group, wl.gamma, alpha)
-        bm = np.zeros((-(-n // b), -(-n // b)), np.uint8)
-        bm[i, :st["mask"].shape[2]] = st["mask"][0, 0]
-        if gpu_mask is not None and (r, h, i) not in seen:
-            seen.add((r, h, i))
-            lr = L[r]
-            row0 = int(mask_off[r]) + (h * lr + i) * lr
-            got = gpu_mask[row0:row0 + st["mask"].shape[2]]
-            want, status = st["mask"][0, 0], st["status"][0, 0]
-            tie = status == O.TIE
-            mchk["block_rows"] += 1
-            mchk["blocks"] += int(want.size)
-            mchk["sure_mismatch"] += int(np.sum((got != want) & ~tie))
-            mchk["tie_blocks"] += int(np.sum(tie))
-            mchk["tie_mismatch"] += int(np.sum((got != want) & tie))
-        tm = O.tile_mask(bm, n, n, b, T, wl.n_local, wl.n_sink, wl.eta, wl.rho, wl.seed, h)
-        tiles = np.flatnonzero(tm[qt])
+        orp, ocols = lists[r]
+        t_q = -(-inp.n[r] // T)
+        row = h * t_q + qt
+        tiles = ocols[orp[row]:orp[row + 1]]
+        kept_sample += int(tiles.size)
+        t0 = time.perf_counter()
+        outs = [O.attention_rows(q, k, v, h * m + pp, qt, T, alpha, tiles)[0] for pp in range(m)]
+        t_attn += time.perf_counter() - t0
+        gr = row_base[r] + row
+        gtiles = gpu_cols[gpu_rp[gr]:gpu_rp[gr + 1]]
         for pp in range(m):
-            o, _ = O.attention_rows(q, k, v, h * m + pp, qt, T, alpha, tiles)
-            g = inp.out_rows(gpu_o, r, h * m + pp, qt * T, qt * T + o.shape[0])
-            max_abs = max(max_abs, float(np.abs(g - o).max()))
-            num += float(((g - o) ** 2).sum())
+            o = outs[pp]
+            if not np.array_equal(gtiles, tiles):
+                o, _ = O.attention_rows(q, k, v, h * m + pp, qt, T, alpha, gtiles)
+            got = inp.out_rows(gpu_o, r, h * m + pp, qt * T, qt * T + o.shape[0])
+            max_abs = max(max_abs, float(np.abs(got - o).max()))
+            num += float(((got - o) ** 2).sum())
             den += float((o ** 2).sum())
-        t_rows = np.arange(qt * T, min(n, (qt + 1) * T))
-        flop += 4.0 * wl.head_dim * m * float((t_rows + 1).sum())
-    dt = time.perf_counter() - t0
-    return {
-        "value": flop / dt / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": int(cores),
+    t_attn_all = t_attn * kept_total / max(kept_sample, 1)
+    total = t_stage1 + t_expand + t_attn_all
+    flop = dense_equiv_flop(inp.n, inp.n, wl.h_q, wl.head_dim)
+    cpu = {
+        "value": flop / total / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": threads,
         "kind": "oracle",
-        "sample": (f"{done} random (request, KV head, q-tile) rows of {len(rows) * wl.h_kv}: "
-                   f"oracle Stage 1 of each row's query block (m={m} heads), its tile stage "
-                   f"and the row's sparse attention; {dt:.1f} s; value = dense-equivalent "
-                   f"FLOP of the sampled rows / oracle time"),
-        "seconds": dt,
-    }, {"max_abs": max_abs, "rel_l2": math.sqrt(num / max(den, 1e-30))}, mchk
+        "sample": (f"whole {wl.name} step on the host: oracle Stage 1 and tile stage in full "
+                   f"({t_stage1:.1f} s + {t_expand:.1f} s), sparse attention of {len(sample)} "
+                   f"stratified (request, KV head, q-tile) rows ({kept_sample} of "
+                   f"{kept_total} kept tiles, {t_attn:.1f} s) extrapolated by kept-tile "
+                   f"count to {t_attn_all:.1f} s; value = dense-equivalent FLOP / total"),
+        "extrapolated": True,
+        "nproc": nproc, "cpu_model": model, "blas_threads": threads,
+        "stage_s": {"estimate_mask": round(t_stage1, 3), "expand_rescue": round(t_expand, 3),
+                    "sparse_prefill_extrapolated": round(t_attn_all, 3)},
+        "attention_sample": {"rows": len(sample), "kept_tiles": kept_sample,
+                             "of_kept_tiles": kept_total, "seconds": round(t_attn, 3)},
+        "seconds_total_extrapolated": round(total, 3),
+    }
+    err = {"max_abs": max_abs, "rel_l2": math.sqrt(num / max(den, 1e-30)),
+           "rows": len(sample)}
+    lchk = {"rows": list_rows, "rows_differ": list_rows_differ}
+    return cpu, err, mchk, lchk
+
+
+class Runner:
+    """One workload's inputs and pass buffers on the GPU, timed with HIP
+    events recorded on the stream the library launches on."""
+
+    def __init__(self, wl, torch, bfla, synth):
+        self.wl, self.torch, self.bfla = wl, torch, bfla
+        t0 = time.perf_counter()
+        self.inp = Inputs(wl, torch, bfla, synth)
+        self.gen_s = time.perf_counter() - t0
+        self.stream = torch.cuda.current_stream()
+
+    def params(self, **over):
+        wl = self.wl
+        kw = dict(block=wl.block, group=wl.group, tile=wl.tile, gamma=wl.gamma,
+                  n_local=wl.n_local, n_sink=wl.n_sink, eta=wl.eta, rho=wl.rho, seed=wl.seed)
+        kw.update(over)
+        return self.bfla.params(**kw)
+
+    def ev(self):
+        return self.torch.cuda.Event(enable_timing=True)
+
+    def step(self, prm, buf, ov, marks=None):
+        bfla, inp = self.bfla, self.inp
+        if marks:
+            marks[0].record(self.stream)
+        bfla.bfla_estimate_mask(inp.prob, prm, inp.qv, inp.kv, buf.block_mask,
+                                dbg_scores=buf.scores)
+        if marks:
+            marks[1].record(self.stream)
+        bfla.bfla_expand_rescue(inp.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
+                                buf.ws_expand)
+        if marks:
+            marks[2].record(self.stream)
+        bfla.bfla_sparse_prefill(inp.prob, prm, inp.qv, inp.kv, buf.row_ptr, buf.cols, ov,
+                                 buf.lse)
+        if marks:
+            marks[3].record(self.stream)
+
+    def lists(self, prm, buf):
+        """One Stage 1 + list pass; the lists are checked on the host before
+        any prefill reads them."""
+        bfla, inp, wl = self.bfla, self.inp, self.wl
+        bfla.bfla_estimate_mask(inp.prob, prm, inp.qv, inp.kv, buf.block_mask,
+                                dbg_scores=buf.scores)
+        bfla.bfla_expand_rescue(inp.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
+                                buf.ws_expand)
+        self.torch.cuda.synchronize()
+        rp = buf.row_ptr.cpu().numpy()
+        cols = buf.cols[:int(rp[-1])].cpu().numpy()
+        assert rp[0] == 0 and np.all(np.diff(rp) >= 0)
+        row = 0
+        for n in inp.n:
+            rows = wl.h_kv * -(-n // wl.tile)
+            seg = cols[rp[row]:rp[row + rows]]
+            assert np.all((seg >= 0) & (seg < -(-n // wl.tile)))
+            row += rows
+        return rp, cols
+
+    def timed(self, prm, buf, ov, steps, warmup):
+        for _ in range(warmup):
+            self.step(prm, buf, ov)
+        marks = [[self.ev() for _ in range(4)] for _ in range(steps)]
+        self.torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        start, end = self.ev(), self.ev()
+        start.record(self.stream)
+        for i in range(steps):
+            self.step(prm, buf, ov, marks[i])
+        end.record(self.stream)
+        self.torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        per_step = {name: [mk[i].elapsed_time(mk[i + 1]) for mk in marks]
+                    for i, name in enumerate(("estimate_mask", "expand_rescue", "sparse_prefill"))}
+        return start.elapsed_time(end) / steps, per_step, wall
+
+    def dense(self, prm, steps):
+        bfla, inp = self.bfla, self.inp
+        bfla.bfla_dense_prefill(inp.prob, prm, inp.qv, inp.kv, inp.odv)
+        self.torch.cuda.synchronize()
+        dm = [(self.ev(), self.ev()) for _ in range(steps)]
+        for a, b in dm:
+            a.record(self.stream)
+            bfla.bfla_dense_prefill(inp.prob, prm, inp.qv, inp.kv, inp.odv)
+            b.record(self.stream)
+        self.torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in dm]))
+
+
+def causal_tile_count(wl, n_tokens):
+    return sum(wl.h_kv * t * (t + 1) // 2 for t in (-(-n // wl.tile) for n in n_tokens))
+
+
+def stage1_record(wl, n_tokens, st1_ms):
+    """Stage 1 (estimate_mask: score GEMM + selection) against both rooflines:
+    algorithmic FLOP over its time vs the MFMA peak, and the score kernel's
+    measured HBM bytes (committed rocprofv3 counters, when they match the
+    kernel source) over the same time vs the HBM peak (a lower bound on the
+    kernel's own rate, since the stage time also holds the selection)."""
+    f1, b1 = stage1_work(n_tokens, n_tokens, wl.h_q, wl.h_kv, wl.head_dim, wl.block, wl.group)
+    t1 = measured_traffic(wl.name, "traffic_bytes_scores")
+    hbm_bytes = t1 if t1 is not None else b1
+    return {"kernels": "scores_kernel + select_kernel (bfla_estimate_mask)",
+            "ms": round(st1_ms, 4), "flop": f1,
+            "achieved_tflops": round(f1 / (st1_ms * 1e-3) / 1e12, 2),
+            "mfma_frac": round(f1 / (st1_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "algorithmic_bytes": b1, "traffic": t1,
+            "hbm_gbs": round(hbm_bytes / (st1_ms * 1e-3) / 1e9, 1),
+            "hbm_bytes_source": "rocprofv3 FETCH+WRITE (profiles/)" if t1 is not None
+            else "algorithmic (Q and K once)",
+            "hbm_frac": round(hbm_bytes / (st1_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "arithmetic_intensity": round(f1 / b1, 1),
+            "bound": "mfma" if f1 / b1 > PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"}
+
+
+def prefill_roofline(wl, kept, pre_ms, traffic):
+    m = wl.h_q // wl.h_kv
+    flop_kept = 4.0 * wl.tile * wl.tile * wl.head_dim * m * kept
+    achieved = flop_kept / (pre_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": "prefill_kernel (sparse)" if wl.head_dim <= 128
+            else "prefill_q16_kernel (sparse)",
+            "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "flop_per_launch": flop_kept,
+            "launch_ms": round(pre_ms, 3),
+            # the other roofline: measured HBM bytes over the same launch time
+            "hbm_gbs": None if traffic is None else round(traffic / (pre_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": None if traffic is None else
+            round(traffic / (pre_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
+def measure(run, steps, warmup, dense_steps):
+    """Headline measurement of one workload: timed passes, the dense baseline,
+    the rooflines and the sparse-vs-dense error."""
+    torch, bfla, wl, inp = run.torch, run.bfla, run.wl, run.inp
+    prm = run.params()
+    buf = bfla.Buffers(inp.prob, prm)
+    rp, cols = run.lists(prm, buf)
+    log(f"{wl.name}: lists valid, {int(rp[-1])} kept tiles")
+    ms_step, per_step, wall = run.timed(prm, buf, inp.ov, steps, warmup)
+    st1 = float(np.mean(per_step["estimate_mask"]))
+    exp_ms = float(np.mean(per_step["expand_rescue"]))
+    pre_ms = float(np.mean(per_step["sparse_prefill"]))
+    log(f"{wl.name}: timed {steps} steps, {ms_step:.3f} ms/step")
+    dense_ms = run.dense(prm, dense_steps)
+    log(f"{wl.name}: dense {dense_ms:.3f} ms")
+    kept = int(rp[-1])
+    flop_dense = dense_equiv_flop(inp.n, inp.n, wl.h_q, wl.head_dim)
+    num = den = 0.0
+    for x in range(0, inp.q.shape[0], 4096):   # chunked to bound temporaries
+        a = inp.o[x:x + 4096].float()
+        b = inp.od[x:x + 4096].float()
+        num += float(torch.sum((a - b) ** 2))
+        den += float(torch.sum(b ** 2))
+    config = {"workload": wl.name, "seq_lens": inp.n, "h_q": wl.h_q, "h_kv": wl.h_kv,
+              "head_dim": wl.head_dim, "block": wl.block, "group": wl.group,
+              "tile": wl.tile, "gamma": wl.gamma, "n_local": wl.n_local,
+              "n_sink": wl.n_sink, "eta": wl.eta, "rho": wl.rho, "seed": wl.seed}
+    if inp.paged:
+        config["kv_layout"] = f"paged, {wl.page_size}-token pages, seeded block table"
+    rec = {
+        "value": round(flop_dense / (ms_step * 1e-3) / 1e12, 2),
+        "ms_per_step": round(ms_step, 3),
+        "config": config,
+        "stage_ms": {"estimate_mask": round(st1, 3), "expand_rescue": round(exp_ms, 3),
+                     "sparse_prefill": round(pre_ms, 3)},
+        "stage_ms_min_median_max": {k: [round(float(np.min(v)), 3), round(float(np.median(v)), 3),
+                                        round(float(np.max(v)), 3)] for k, v in per_step.items()},
+        "dense_ms": round(dense_ms, 3),
+        "dense_tflops": round(flop_dense / (dense_ms * 1e-3) / 1e12, 2),
+        "speedup_vs_dense": round(dense_ms / ms_step, 3),
+        "keep_ratio": round(kept / causal_tile_count(wl, inp.n), 5),
+        "kept_tiles": kept,
+        "sparse_vs_dense_rel_l2": round(math.sqrt(num / max(den, 1e-30)), 5),
+        "roofline": prefill_roofline(wl, kept, pre_ms, measured_traffic(wl.name)),
+        "stage1_roofline": stage1_record(wl, inp.n, st1),
+        "wall_s_timed": round(wall, 3),
+        "input_gen_s": round(run.gen_s, 1),
+    }
+    host = {"mask": buf.block_mask.cpu().numpy(), "rp": rp, "cols": cols}
+    return rec, host, dense_ms
+
+
+def sweep(run, dense_ms, steps, points):
+    """The same workload at other thresholds gamma and random-rescue rates rho:
+    keep ratio, stage times, speedup over the dense prefill (timed once: it
+    does not depend on gamma or rho) and the kept-tile MFMA fraction."""
+    wl, inp = run.wl, run.inp
+    out = []
+    flop_dense = dense_equiv_flop(inp.n, inp.n, wl.h_q, wl.head_dim)
+    buf = o = None
+    for gamma, rho in points:
+        prm = run.params(gamma=gamma, rho=rho)
+        if buf is None:
+            buf = run.bfla.Buffers(inp.prob, prm)
+            o = run.torch.empty_like(inp.o)
+            ov = (run.bfla.view_hnc(o) if not inp.paged
+                  else run.bfla.view_packed(o, inp.starts))
+        rp, _ = run.lists(prm, buf)
+        ms_step, per_step, _ = run.timed(prm, buf, ov, steps, 1)
+        pre = float(np.mean(per_step["sparse_prefill"]))
+        kept = int(rp[-1])
+        rf = prefill_roofline(wl, kept, pre, None)
+        out.append({"gamma": gamma, "rho": rho,
+                    "keep_ratio": round(kept / causal_tile_count(wl, inp.n), 5),
+                    "kept_tiles": kept,
+                    "stage_ms": {k: round(float(np.mean(v)), 3) for k, v in per_step.items()},
+                    "ms_per_step": round(ms_step, 3),
+                    "speedup_vs_dense": round(dense_ms / ms_step, 3),
+                    "dense_equiv_tflops": round(flop_dense / (ms_step * 1e-3) / 1e12, 2),
+                    "kept_tile_tflops": rf["achieved"], "kept_tile_frac": rf["frac"]})
+        log(f"sweep gamma {gamma} rho {rho}: keep {out[-1]['keep_ratio']:.4f}, "
+            f"{ms_step:.3f} ms/step, {out[-1]['speedup_vs_dense']:.2f}x")
+    return out
 
 
 def main():
@@ -269,79 +567,10 @@ def main():
         if val is not None:
             over[key] = val
     wl = synth.workload(args.workload, **over)
-    t_gen = time.perf_counter()
     torch.cuda.set_device(0)
-    inp = Inputs(wl, torch, bfla, synth)
-    t_gen = time.perf_counter() - t_gen
-    log(f"{wl.name}: inputs ready in {t_gen:.1f} s")
-    prob = inp.prob
-    prm = bfla.params(block=wl.block, group=wl.group, tile=wl.tile, gamma=wl.gamma,
-                      n_local=wl.n_local, n_sink=wl.n_sink, eta=wl.eta, rho=wl.rho,
-                      seed=wl.seed)
-    buf = bfla.Buffers(prob, prm)
-    stream = torch.cuda.current_stream()
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-
-    def step(marks=None):
-        if marks:
-            marks[0].record(stream)
-        bfla.bfla_estimate_mask(prob, prm, inp.qv, inp.kv, buf.block_mask, dbg_scores=buf.scores)
-        if marks:
-            marks[1].record(stream)
-        bfla.bfla_expand_rescue(prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
-        if marks:
-            marks[2].record(stream)
-        bfla.bfla_sparse_prefill(prob, prm, inp.qv, inp.kv, buf.row_ptr, buf.cols, inp.ov,
-                                 buf.lse)
-        if marks:
-            marks[3].record(stream)
-
-    # first pass: validate the lists on the host before timing anything
-    bfla.bfla_estimate_mask(prob, prm, inp.qv, inp.kv, buf.block_mask, dbg_scores=buf.scores)
-    bfla.bfla_expand_rescue(prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
-    torch.cuda.synchronize()
-    rp = buf.row_ptr.cpu().numpy()
-    cols_h = buf.cols[:int(rp[-1])].cpu().numpy()
-    assert rp[0] == 0 and np.all(np.diff(rp) >= 0)
-    row = 0
-    for n in inp.n:
-        rows = wl.h_kv * -(-n // wl.tile)
-        seg = cols_h[rp[row]:rp[row + rows]]
-        assert np.all((seg >= 0) & (seg < -(-n // wl.tile)))
-        row += rows
-    log(f"lists valid: {int(rp[-1])} kept tiles")
-
-    for _ in range(args.warmup):
-        step()
-    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start, end = ev(), ev()
-    start.record(stream)
-    for i in range(args.steps):
-        step(marks[i])
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = start.elapsed_time(end) / args.steps
-    per_step = {name: [m[i].elapsed_time(m[i + 1]) for m in marks]
-                for i, name in enumerate(("estimate_mask", "expand_rescue", "sparse_prefill"))}
-    st1 = float(np.mean(per_step["estimate_mask"]))
-    exp_ms = float(np.mean(per_step["expand_rescue"]))
-    pre_ms = float(np.mean(per_step["sparse_prefill"]))
-    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
-
-    # dense baseline (same kernel family, every causal tile)
-    bfla.bfla_dense_prefill(prob, prm, inp.qv, inp.kv, inp.odv)
-    torch.cuda.synchronize()
-    dm = [(ev(), ev()) for _ in range(args.dense_steps)]
-    for a, b in dm:
-        a.record(stream)
-        bfla.bfla_dense_prefill(prob, prm, inp.qv, inp.kv, inp.odv)
-        b.record(stream)
-    torch.cuda.synchronize()
-    dense_ms = float(np.mean([a.elapsed_time(b) for a, b in dm]))
-    log(f"dense {dense_ms:.3f} ms")
+    run = Runner(wl, torch, bfla, synth)
+    log(f"{wl.name}: inputs ready in {run.gen_s:.1f} s")
+    rec, host, dense_ms = measure(run, args.steps, args.warmup, args.dense_steps)
     if args.calib_copy_mib > 0:
         nbytes = args.calib_copy_mib << 20
         src = torch.ones(nbytes, dtype=torch.uint8, device="cuda:0")
@@ -352,93 +581,40 @@ def main():
         log(f"calibration copy of {args.calib_copy_mib} MiB done")
         del src, dst
 
-    kept = int(rp[-1])
-    causal_tiles = sum(wl.h_kv * t * (t + 1) // 2 for t in (-(-n // wl.tile) for n in inp.n))
-    m = wl.h_q // wl.h_kv
-    flop_dense = dense_equiv_flop(inp.n, inp.n, wl.h_q, wl.head_dim)
-    flop_kept = 4.0 * wl.tile * wl.tile * wl.head_dim * m * kept
-    achieved = flop_kept / (pre_ms * 1e-3) / 1e12
-    num = den = 0.0
-    for x in range(0, inp.q.shape[0], 4096):   # chunked to bound temporaries
-        a = inp.o[x:x + 4096].float()
-        b = inp.od[x:x + 4096].float()
-        num += float(torch.sum((a - b) ** 2))
-        den += float(torch.sum(b ** 2))
-    sd_err = math.sqrt(num / max(den, 1e-30))
-
-    # Stage 1 (estimate_mask: score GEMM + selection) against both rooflines:
-    # algorithmic FLOP over its time vs the MFMA peak, and the score kernel's
-    # measured HBM bytes (committed rocprofv3 counters) over the same time vs
-    # the HBM peak (a lower bound on the kernel's own rate, since the stage
-    # time also holds the selection kernel)
-    f1, b1 = stage1_work(inp.n, inp.n, wl.h_q, wl.h_kv, wl.head_dim, wl.block, wl.group)
-    t1 = measured_traffic(wl.name, "traffic_bytes_scores")
-    hbm_bytes = t1 if t1 is not None else b1
-    stage1 = {"kernels": "scores_kernel + select_kernel (bfla_estimate_mask)",
-              "ms": round(st1, 4), "flop": f1,
-              "achieved_tflops": round(f1 / (st1 * 1e-3) / 1e12, 2),
-              "mfma_frac": round(f1 / (st1 * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-              "algorithmic_bytes": b1, "traffic": t1,
-              "hbm_gbs": round(hbm_bytes / (st1 * 1e-3) / 1e9, 1),
-              "hbm_bytes_source": "rocprofv3 FETCH+WRITE (profiles/)" if t1 is not None
-              else "algorithmic (Q and K once)",
-              "hbm_frac": round(hbm_bytes / (st1 * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-              "arithmetic_intensity": round(f1 / b1, 1),
-              "bound": "mfma" if f1 / b1 > PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"}
-
-    traffic = measured_traffic(wl.name)
-
-    config = {"workload": wl.name, "seq_lens": inp.n, "h_q": wl.h_q, "h_kv": wl.h_kv,
-              "head_dim": wl.head_dim, "block": wl.block, "group": wl.group,
-              "tile": wl.tile, "gamma": wl.gamma, "n_local": wl.n_local,
-              "n_sink": wl.n_sink, "eta": wl.eta, "rho": wl.rho, "seed": wl.seed}
-    if inp.paged:
-        config["kv_layout"] = f"paged, {wl.page_size}-token pages, seeded block table"
     result = {
         "metric": METRIC,
-        "value": round(flop_dense / (ms_step * 1e-3) / 1e12, 2),
+        "value": rec.pop("value"),
         "unit": "TFLOP/s (dense-equivalent)",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3),
+        "ms_per_step": rec.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) with planted sinks and heavy hitters)",
-        "config": config,
-        "stage_ms": {"estimate_mask": round(st1, 3), "expand_rescue": round(exp_ms, 3),
-                     "sparse_prefill": round(pre_ms, 3)},
-        "stage_ms_min_median_max": {k: [round(float(np.min(v)), 3), round(float(np.median(v)), 3),
-                                        round(float(np.max(v)), 3)] for k, v in per_step.items()},
-        "dense_ms": round(dense_ms, 3),
-        "dense_tflops": round(flop_dense / (dense_ms * 1e-3) / 1e12, 2),
-        "speedup_vs_dense": round(dense_ms / ms_step, 3),
-        "keep_ratio": round(kept / causal_tiles, 5),
-        "kept_tiles": kept,
-        "sparse_vs_dense_rel_l2": round(sd_err, 5),
-        "roofline": {"bound": "mfma", "kernel": "prefill_kernel (sparse)",
-                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic,
-                     "flop_per_launch": flop_kept,
-                     "launch_ms": round(pre_ms, 3),
-                     # the other roofline: measured HBM bytes over the same launch time
-                     "hbm_gbs": None if traffic is None else round(traffic / (pre_ms * 1e-3) / 1e9, 1),
-                     "hbm_frac": None if traffic is None else
-                     round(traffic / (pre_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
-        "stage1_roofline": stage1,
-        "wall_s_timed": round(wall, 3),
-        "input_gen_s": round(t_gen, 1),
+        "config": rec.pop("config"),
     }
+    result.update(rec)
+    headline = not args.only and args.workload == "llama_128k" and not over
     if not args.no_cpu:
-        cpu, err, mchk = cpu_baseline(wl, inp, inp.o, args.cpu_seconds,
-                                      gpu_mask=buf.block_mask.cpu().numpy())
-        log(f"cpu baseline {cpu['seconds']:.1f} s")
-        result["cpu_baseline"] = {kk: vv for kk, vv in cpu.items() if kk != "seconds"}
-        result["rel_err_vs_oracle_sampled"] = {kk: round(vv, 6) for kk, vv in err.items()}
-        result["mask_vs_oracle_sampled"] = mchk
+        cpu, err, mchk, lchk = cpu_baseline(wl, run.inp, run.inp.o, host["mask"], host["rp"],
+                                            host["cols"], rows=args.cpu_rows)
+        log(f"cpu baseline: {cpu['seconds_total_extrapolated']:.1f} s per step (extrapolated)")
+        result["cpu_baseline"] = cpu
+        result["rel_err_vs_oracle_sampled"] = {kk: (round(vv, 6) if isinstance(vv, float) else vv)
+                                               for kk, vv in err.items()}
+        result["mask_vs_oracle"] = mchk
+        result["lists_vs_oracle"] = lchk
+    if headline:
+        pts = [(g, r) for g in (0.8, 0.9, 0.95) for r in (0.0, 0.1)]
+        result["sweep_128k"] = sweep(run, dense_ms, args.sweep_steps, pts)
+        del run
+        torch.cuda.empty_cache()
+        run32 = Runner(synth.workload("llama_32k"), torch, bfla, synth)
+        rec32, _, _ = measure(run32, args.steps, args.warmup, args.dense_steps)
+        result["llama_32k"] = rec32
     print(json.dumps(result), flush=True)
 
 

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define BFLA_VERSION_STRING "0.1.0"
+#define BFLA_VERSION_STRING "0.2.0"
 /* Maximum number of requests per call (descriptors travel in kernel
  * arguments). */
 #define BFLA_MAX_BATCH 32
@@ -142,6 +142,9 @@ typedef struct bfla_params {
  *              1 = keep, 0 = drop (also every non-causal cell).
  *  dbg_scores  float [H_q][L_q][L_kv] per request (block scores S of eq10,
  *              -inf where not causal, eq14).
+ *  dbg_head_mask  uint8 [H_q][L_q][L_kv] per request, at the same element
+ *              offsets as dbg_scores: the keep set of each query head
+ *              before the GQA union (eq18), 1 = kept by that head.
  *  lists       rows ordered (request, KV head, q-tile): row index
  *              sum_{r'<r} H_kv*T_q(r') + h*T_q(r) + qt, T_q = ceil(N_q/T).
  *              row_ptr int32 [n_rows + 1] (row_ptr[0] = 0), cols int32
@@ -173,11 +176,14 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
  * shortest prefix of blocks in descending order whose mass reaches gamma
  * (eq16-eq18; ties: lower block index first; gamma >= 1 keeps all causal
  * blocks); OR over the m query heads of each KV head.
- *   q           Q view (bf16).
- *   kv          K (and V, unused here) descriptor.
- *   block_mask  out, device uint8, layout above.
- *   dbg_scores  out, device float or NULL.
- *   workspace   device scratch of >= bfla_workspace_size(BFLA_WS_ESTIMATE).
+ *   q              Q view (bf16).
+ *   kv             K (and V, unused here) descriptor.
+ *   block_mask     out, device uint8, layout above.
+ *   dbg_scores     out, device float or NULL (then the workspace holds them).
+ *   dbg_head_mask  out, device uint8 or NULL: the per-query-head keep sets
+ *                  of eq18 that the union combines (layout above).
+ *   workspace      device scratch of >= bfla_workspace_size(BFLA_WS_ESTIMATE)
+ *                  (unused, and may be NULL, when dbg_scores is given).
  * Errors: INVALID_ARG, UNSUPPORTED (also: m > 8; more than 65536 KV blocks
  * per request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
  * i.e. (128 g - 1) * stride_tok + head_dim >= 2^30; paged K where 128 g
@@ -185,7 +191,8 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
 int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params,
                        const bfla_view* q, const bfla_kv* kv,
                        uint8_t* block_mask, float* dbg_scores,
-                       void* workspace, size_t ws_bytes, void* stream);
+                       uint8_t* dbg_head_mask, void* workspace,
+                       size_t ws_bytes, void* stream);
 
 /* Stage 2 tile mask, eq19-eq26: tile (qt, kt) of KV head h inherits block
  * (qt / (b/T), kt / (b/T)) of block_mask, clipped to causal tiles; the

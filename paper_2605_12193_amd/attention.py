@@ -27,10 +27,15 @@ def _layout(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor):
     for name, t in (("q", q), ("k", k), ("v", v)):
         if t.dtype != torch.bfloat16:
             raise ValueError(f"{name} must be bfloat16, got {t.dtype}")
-        if not t.is_cuda:
-            raise ValueError(f"{name} must be on the GPU")
         if t.stride(-1) != 1:
             raise ValueError(f"{name} must have a contiguous last dimension")
+    # the library addresses K and V with one set of strides
+    if v.stride() != k.stride():
+        raise ValueError(f"v strides {tuple(v.stride())} differ from k strides "
+                         f"{tuple(k.stride())}")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
     batch = q.shape[0] if q.dim() == 4 else 1
     h_q, n_q, c = q.shape[-3:]
     h_kv, n_kv, c_k = k.shape[-3:]

@@ -15,41 +15,14 @@ from typing import List, Optional, Sequence
 
 import torch
 
+from .abi import (BFLA_ERR_CAPACITY, BFLA_ERR_HIP, BFLA_ERR_INVALID_ARG,  # noqa: F401
+                  BFLA_ERR_UNSUPPORTED, BFLA_ERR_WORKSPACE, BFLA_KV_CONTIGUOUS, BFLA_KV_PAGED,
+                  BFLA_OK, BFLA_WS_ESTIMATE, BFLA_WS_EXPAND, EXPORTS, MAX_BATCH, bfla_kv,
+                  bfla_params, bfla_problem, bfla_view)
+from .abi import SIGS as _SIGS  # noqa: F401
+from .abi import bind as _bind
+
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbfla.so")
-
-BFLA_OK, BFLA_ERR_INVALID_ARG, BFLA_ERR_UNSUPPORTED = 0, 1, 2
-BFLA_ERR_WORKSPACE, BFLA_ERR_CAPACITY, BFLA_ERR_HIP = 3, 4, 5
-BFLA_KV_CONTIGUOUS, BFLA_KV_PAGED = 0, 1
-BFLA_WS_ESTIMATE, BFLA_WS_EXPAND = 1, 2
-MAX_BATCH = 32
-
-
-class bfla_problem(C.Structure):
-    _fields_ = [("batch", C.c_int32), ("h_q", C.c_int32), ("h_kv", C.c_int32),
-                ("head_dim", C.c_int32), ("n_q", C.POINTER(C.c_int32)),
-                ("n_kv", C.POINTER(C.c_int32))]
-
-
-class bfla_view(C.Structure):
-    _fields_ = [("data", C.c_void_p), ("batch_offset", C.POINTER(C.c_int64)),
-                ("stride_batch", C.c_int64), ("stride_head", C.c_int64),
-                ("stride_tok", C.c_int64)]
-
-
-class bfla_kv(C.Structure):
-    _fields_ = [("layout", C.c_int32), ("k", C.c_void_p), ("v", C.c_void_p),
-                ("batch_offset", C.POINTER(C.c_int64)), ("stride_batch", C.c_int64),
-                ("stride_head", C.c_int64), ("stride_tok", C.c_int64),
-                ("page_size", C.c_int32), ("max_pages", C.c_int32),
-                ("page_stride", C.c_int64), ("block_table", C.c_void_p),
-                ("n_pages", C.c_int64)]
-
-
-class bfla_params(C.Structure):
-    _fields_ = [("block", C.c_int32), ("group", C.c_int32), ("tile", C.c_int32),
-                ("gamma", C.c_float), ("n_local", C.c_int32), ("n_sink", C.c_int32),
-                ("eta", C.c_int32), ("rho", C.c_double), ("seed", C.c_uint64),
-                ("scale", C.c_float)]
 
 
 class BflaError(RuntimeError):
@@ -60,30 +33,6 @@ class BflaError(RuntimeError):
 
 _lib = None
 
-_SIGS = {
-    "bfla_workspace_size": [C.POINTER(bfla_problem), C.POINTER(bfla_params), C.c_int,
-                            C.POINTER(C.c_size_t)],
-    "bfla_list_capacity": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
-                           C.POINTER(C.c_size_t), C.POINTER(C.c_size_t),
-                           C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)],
-    "bfla_estimate_mask": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
-                           C.POINTER(bfla_view), C.POINTER(bfla_kv), C.c_void_p,
-                           C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p],
-    "bfla_expand_rescue": [C.POINTER(bfla_problem), C.POINTER(bfla_params), C.c_void_p,
-                           C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p, C.c_size_t,
-                           C.c_void_p],
-    "bfla_sparse_prefill": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
-                            C.POINTER(bfla_view), C.POINTER(bfla_kv), C.c_void_p,
-                            C.c_void_p, C.POINTER(bfla_view), C.c_void_p, C.c_void_p],
-    "bfla_dense_prefill": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
-                           C.POINTER(bfla_view), C.POINTER(bfla_kv),
-                           C.POINTER(bfla_view), C.c_void_p, C.c_void_p],
-    "bfla_status_string": [C.c_int],
-    "bfla_last_error": [],
-    "bfla_version": [],
-}
-EXPORTS = tuple(_SIGS)
-
 
 def lib():
     """The loaded library (raises if it was not built)."""
@@ -92,13 +41,7 @@ def lib():
         if not os.path.exists(_LIB_PATH):
             raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
                                "`python -m paper_2605_12193_amd.build`")
-        L = C.CDLL(_LIB_PATH)
-        for name, args in _SIGS.items():
-            fn = getattr(L, name)
-            fn.argtypes = args
-            fn.restype = C.c_char_p if name in ("bfla_status_string", "bfla_last_error",
-                                                "bfla_version") else C.c_int
-        _lib = L
+        _lib = _bind(_LIB_PATH)
     return _lib
 
 
@@ -166,9 +109,25 @@ def view_packed(t: torch.Tensor, token_starts: Sequence[int]) -> View:
 
 
 class KV:
+    """bfla_kv of K and V, which share one set of strides (the library reads
+    both through the same addressing); a paged table is int32 [B][max_pages]."""
+
     def __init__(self, k: torch.Tensor, v: torch.Tensor, *, paged: bool = False,
                  block_table: Optional[torch.Tensor] = None,
                  batch_offsets: Optional[Sequence[int]] = None):
+        if k.shape != v.shape or k.stride() != v.stride():
+            raise ValueError(f"k {tuple(k.shape)}/{tuple(k.stride())} and v "
+                             f"{tuple(v.shape)}/{tuple(v.stride())} need the same shape "
+                             "and strides")
+        if paged:
+            if k.dim() != 4:
+                raise ValueError("paged k / v must be [pages][page_size][H_kv][C]")
+            if block_table is None or block_table.dtype != torch.int32 \
+                    or block_table.dim() != 2 or not block_table.is_contiguous():
+                raise ValueError("block_table must be a contiguous int32 [batch][max_pages] "
+                                 "tensor")
+            if block_table.device != k.device:
+                raise ValueError("block_table must be on the same device as k / v")
         self.k, self.v, self.block_table = k, v, block_table
         self._off = None
         if paged:
@@ -221,11 +180,12 @@ def bfla_workspace_size(prob: Problem, prm: bfla_params, which: int) -> int:
 
 def bfla_estimate_mask(prob: Problem, prm: bfla_params, q: View, kv: KV,
                        block_mask: torch.Tensor, dbg_scores: Optional[torch.Tensor] = None,
+                       dbg_head_mask: Optional[torch.Tensor] = None,
                        workspace: Optional[torch.Tensor] = None, stream=None) -> None:
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().bfla_estimate_mask(C.byref(prob.c), C.byref(prm), C.byref(q.c), C.byref(kv.c),
-                                    _ptr(block_mask), _ptr(dbg_scores), _ptr(workspace),
-                                    ws_bytes, _stream(stream)))
+                                    _ptr(block_mask), _ptr(dbg_scores), _ptr(dbg_head_mask),
+                                    _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def bfla_expand_rescue(prob: Problem, prm: bfla_params, block_mask: torch.Tensor,

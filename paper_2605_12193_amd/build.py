@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbfla.so")
 
-SOURCES = ["api.cpp", "prefill.hip", "expand.hip", "estimate.hip"]
+SOURCES = ["api.cpp", "shapes.cpp", "prefill.hip", "expand.hip", "estimate.hip"]
 
 # Packed fp32 VALU ops are disabled for every device pass; hipcc's host pass
 # warns that it does not know the feature, which is harmless.

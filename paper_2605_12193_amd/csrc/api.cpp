@@ -336,7 +336,8 @@ int bfla_workspace_size(const bfla_problem* prob, const bfla_params* params, int
 
 int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, const bfla_view* q,
                        const bfla_kv* kv, uint8_t* block_mask, float* dbg_scores,
-                       void* workspace, size_t ws_bytes, void* stream) {
+                       uint8_t* dbg_head_mask, void* workspace, size_t ws_bytes,
+                       void* stream) {
   int st;
   if ((st = check_problem(prob, params))) return st;
   if ((st = check_view(prob, q, "q"))) return st;
@@ -373,6 +374,7 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   L.kv = kv_addr(kv);
   L.block_mask = block_mask;
   L.scores = scores;
+  L.head_mask = dbg_head_mask;
   L.h_q = prob->h_q;
   L.h_kv = prob->h_kv;
   L.head_dim = prob->head_dim;

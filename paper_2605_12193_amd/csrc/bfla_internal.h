@@ -1,4 +1,6 @@
 // Host-side launcher interface between the C ABI (api.cpp) and the kernels.
+// The shape predicates and workspace sizes are host code (shapes.cpp); the
+// launch_* functions live beside their kernels.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -6,6 +8,14 @@
 #include "bfla_device.h"
 
 namespace bfla {
+
+// Stage-1 score tiles: kScoreTileM query groups x kScoreTileN key groups,
+// kScoreChunk inner elements per LDS stage; the page numbers one tile of a
+// paged cache spans are resolved into LDS, at most kScorePagesMax of them.
+constexpr int kScoreTileM = 256;
+constexpr int kScoreTileN = 128;
+constexpr int kScoreChunk = 64;
+constexpr int kScorePagesMax = 2048;
 
 struct PrefillLaunch {
   const void* q;
@@ -49,6 +59,7 @@ struct EstimateLaunch {
   KvAddr kv;
   uint8_t* block_mask;
   float* scores;      // [per request H_q x L_q x L_kv], workspace or dbg output
+  uint8_t* head_mask; // [per request H_q x L_q x L_kv] per-head keep sets, or null
   int32_t h_q, h_kv, head_dim;
   int32_t block, group;
   float gamma;
@@ -58,7 +69,7 @@ struct EstimateLaunch {
 
 bool estimate_supported(int head_dim, int block, int group);
 // Stage-1 address limits: the query rows of one score tile must span < 2 GiB,
-// and one tile's keys of a paged cache at most PT_MAX pages.
+// and one tile's keys of a paged cache at most kScorePagesMax pages.
 bool estimate_q_fits(int group, int head_dim, int64_t q_stride_tok);
 bool estimate_pages_fit(int group, int page_size);
 hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream);

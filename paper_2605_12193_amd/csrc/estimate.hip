@@ -20,15 +20,16 @@
 // blocks (eq15), keep-mass selection by repeated arg-max in the order
 // (score descending, block index ascending) with a sequential float
 // running mass (eq16-eq18), then OR of the m heads into the u8 mask row.
+// On request each wave also stores its own head's keep set (eq18).
 #include "bfla_device.h"
 #include "bfla_internal.h"
 
 namespace bfla {
 namespace {
 
-constexpr int BM = 256;     // query groups per tile (32 per wave)
-constexpr int BN = 128;     // key groups per tile
-constexpr int BK = 64;      // inner elements per stage
+constexpr int BM = kScoreTileM;   // query groups per tile (32 per wave)
+constexpr int BN = kScoreTileN;   // key groups per tile
+constexpr int BK = kScoreChunk;   // inner elements per stage
 // 8 waves (two per SIMD): each keeps its own DMA loads in flight, and the
 // kernel is bound by the memory requests in flight (4 waves of 64 x 128
 // outputs each were 12 % slower)
@@ -53,6 +54,7 @@ struct SelectArgs {
   const float* scores;
   float* dbg;        // non-null: also fill non-causal entries with -inf
   uint8_t* block_mask;
+  uint8_t* head_mask;  // non-null: per-query-head keep sets, score layout
   int32_t h_q, h_kv, m, b;
   float gamma, alpha;
   Batch batch;       // work_begin = first (h, i) row of request r
@@ -80,7 +82,7 @@ constexpr int A_LOADS = BM / 8 / NW;   // 1 KB loads per wave per stage (8 rows 
 constexpr int B_LOADS = BN / 8 / NW;
 constexpr int VM_STAGE = A_LOADS + B_LOADS;
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;
-constexpr int PT_MAX = 2048;  // page-table entries one tile of a paged cache may span
+constexpr int PT_MAX = kScorePagesMax;  // page-table entries one tile of a paged cache may span
 constexpr uint32_t BAD_PAGE = 0xFFFFFFFFu;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
@@ -365,6 +367,14 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
   const int n_causal = e_i / a.b + 1;
   const int words = (R.l_kv + 31) / 32;
 
+  // this head's own keep set: cleared here (every head keeps all causal
+  // blocks when gamma >= 1); the barrier below orders these stores before
+  // the picks that lane 0 stores during the selection
+  uint8_t* hrow = a.head_mask
+                      ? a.head_mask + R.score_off + ((int64_t)p * R.l_q + i) * R.l_kv
+                      : nullptr;
+  if (hrow)
+    for (int j = lane; j < R.l_kv; j += 64) hrow[j] = (a.gamma >= 1.0f && j < n_causal) ? 1 : 0;
   for (int w = tid; w < words; w += blockDim.x) keep_bits[w] = 0u;
   __syncthreads();
 
@@ -420,7 +430,10 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
         if (better(os, oj, bs, bj)) { bs = os; bj = oj; }
       }
       if (bj >= n_causal) break;  // only with non-finite scores: nothing left to rank
-      if (lane == 0) atomicOr(&keep_bits[bj >> 5], 1u << (bj & 31));
+      if (lane == 0) {
+        atomicOr(&keep_bits[bj >> 5], 1u << (bj & 31));
+        if (hrow) hrow[bj] = 1;
+      }
       mass += expf(a.alpha * (bs - mx)) / z;
       if (mass >= a.gamma) break;
       s_prev = bs;
@@ -447,23 +460,6 @@ hipError_t launch_scores(const ScoreArgs& a, int n_tiles, hipStream_t s) {
 }
 
 }  // namespace
-
-bool estimate_supported(int head_dim, int block, int group) {
-  if (head_dim != 64 && head_dim != 128 && head_dim != 256) return false;
-  if (group < 1 || block % group) return false;
-  const int G = block / group;
-  if (G != 1 && G != 2 && G != 4 && G != 8 && G != 16) return false;
-  return ((int64_t)group * head_dim) % BK == 0;
-}
-
-bool estimate_q_fits(int group, int head_dim, int64_t q_stride_tok) {
-  return ((int64_t)BM * group - 1) * q_stride_tok + head_dim < (int64_t(1) << 30);
-}
-
-bool estimate_pages_fit(int group, int page_size) {
-  // a tile of BN key groups covers BN * g tokens: at most BN * g / ps + 1 pages
-  return ((int64_t)BN * group + page_size - 1) / page_size + 1 <= PT_MAX;
-}
 
 hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
   const int m = L.h_q / L.h_kv;
@@ -506,6 +502,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
   s.scores = L.scores;
   s.dbg = L.scores;  // always fill the non-causal entries (cheap, defined output)
   s.block_mask = L.block_mask;
+  s.head_mask = L.head_mask;
   s.h_q = L.h_q;
   s.h_kv = L.h_kv;
   s.m = m;

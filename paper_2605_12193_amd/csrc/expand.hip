@@ -156,13 +156,6 @@ __global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a)
 
 }  // namespace
 
-// counts [n_rows rounded up to 64] + scan partials [64] (int32), then the
-// ballots [n_rows][ceil(max_t_kv / 64)] (uint64, 256-byte aligned offset)
-size_t expand_workspace_bytes(int64_t n_rows, int64_t max_t_kv) {
-  return (size_t)(((n_rows + 63) / 64) * 64 + 64) * sizeof(int32_t) +
-         (size_t)n_rows * (size_t)((max_t_kv + 63) / 64) * sizeof(uint64_t);
-}
-
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
   if (L.n_rows == 0) return hipSuccess;
   ExpandArgs a;

@@ -1309,12 +1309,6 @@ hipError_t launch_c(const PrefillArgs& a, bool dense, int n_work, hipStream_t s)
 
 }  // namespace
 
-bool prefill_supported(int head_dim, int m) {
-  bool c_ok = head_dim == 64 || head_dim == 128 || head_dim == 256;
-  bool m_ok = m >= 1 && m <= 8;
-  return c_ok && m_ok;
-}
-
 hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
   PrefillArgs a;
   a.q = static_cast<const bf16_t*>(L.q);

@@ -1,5 +1,7 @@
 """Helpers shared by the GPU parity tests: device packing of seeded inputs,
-calls through the C ABI, and the comparison bars."""
+calls through the C ABI, the comparison bars, and canary bands around every
+output buffer (4 KiB of a fixed byte pattern before and after it, checked
+after each entry point: a write out of bounds changes a band)."""
 from __future__ import annotations
 
 import numpy as np
@@ -11,6 +13,59 @@ from paper_2605_12193_amd import bfla, synth
 # Output bar for bf16 outputs against the float64 oracle on the same lists.
 MAX_ABS = 2e-2
 REL_L2 = 5e-3
+
+GUARD_BYTES = 4096
+GUARD_BYTE = 0xA5
+
+
+class Guarded:
+    """A device buffer of n elements between two 4 KiB canary bands; ``t`` is
+    the buffer itself (16-byte aligned like any fresh allocation)."""
+
+    def __init__(self, n, dtype, fill=None, device="cuda"):
+        item = torch.empty((), dtype=dtype).element_size()
+        pad = GUARD_BYTES // item
+        self._raw = torch.empty(n + 2 * pad, dtype=dtype, device=device)
+        self._raw.view(torch.uint8).fill_(GUARD_BYTE)
+        self.t = self._raw[pad:pad + n]
+        if fill is not None:
+            self.t.fill_(fill)
+
+    def check(self, what):
+        b = self._raw.view(torch.uint8)
+        for name, band in (("before", b[:GUARD_BYTES]), ("after", b[-GUARD_BYTES:])):
+            bad = torch.nonzero(band != GUARD_BYTE).flatten()
+            assert bad.numel() == 0, (f"{what}: canary band {name} the buffer overwritten at "
+                                      f"{bad[:8].tolist()} ({bad.numel()} bytes)")
+
+
+class GuardedBuffers:
+    """The buffers of one pass (as bfla.Buffers), each between canary bands;
+    optionally the per-query-head keep sets of Stage 1."""
+
+    def __init__(self, prob, prm, head_mask=False):
+        cap = bfla.bfla_list_capacity(prob, prm)
+        self.cap = cap
+        ws = bfla.bfla_workspace_size(prob, prm, bfla.BFLA_WS_EXPAND)
+        n_lse = sum(prob.c.h_q * n for n in prob.n_q)
+        self.g = {
+            "block_mask": Guarded(max(cap.mask_bytes, 1), torch.uint8, fill=9),
+            "scores": Guarded(max(cap.score_elems, 1), torch.float32, fill=float("nan")),
+            "row_ptr": Guarded(cap.n_rows + 1, torch.int32, fill=-5),
+            "cols": Guarded(max(cap.max_cols, 1), torch.int32, fill=-7),
+            "ws_expand": Guarded(max(ws, 16), torch.uint8),
+            "lse": Guarded(n_lse, torch.float32, fill=float("nan")),
+        }
+        if head_mask:
+            self.g["head_mask"] = Guarded(max(cap.score_elems, 1), torch.uint8, fill=9)
+        for k, v in self.g.items():
+            setattr(self, k, v.t)
+        if not head_mask:
+            self.head_mask = None
+
+    def check(self, what=""):
+        for k, v in self.g.items():
+            v.check(f"{what} {k}")
 
 
 class DeviceBatch:
@@ -28,7 +83,8 @@ class DeviceBatch:
         self.q = torch.cat(qs, dim=1).contiguous().cuda()
         self.k = torch.cat([s.k for s in seqs], dim=1).contiguous().cuda()
         self.v = torch.cat([s.v for s in seqs], dim=1).contiguous().cuda()
-        self.o = torch.full_like(self.q, float("nan"))
+        self.o_guard = Guarded(self.q.numel(), self.q.dtype, fill=float("nan"))
+        self.o = self.o_guard.t.view(self.q.shape)
         self.q_start = np.concatenate([[0], np.cumsum(self.n_q)[:-1]]).astype(int)
         self.kv_start = np.concatenate([[0], np.cumsum(self.n_kv)[:-1]]).astype(int)
         self.prob = bfla.Problem(self.n_q, self.n_kv, h_q, h_kv, c)
@@ -60,7 +116,8 @@ class PagedBatch:
         h_kv = seqs[0].k.shape[0]
         qs = [s.q[:, s.q.shape[1] - nq:].transpose(0, 1) for s, nq in zip(seqs, self.n_q)]
         self.q = torch.cat(qs, dim=0).contiguous().cuda()          # [sum N_q][H_q][C]
-        self.o = torch.full_like(self.q, float("nan"))
+        self.o_guard = Guarded(self.q.numel(), self.q.dtype, fill=float("nan"))
+        self.o = self.o_guard.t.view(self.q.shape)
         starts = np.concatenate([[0], np.cumsum(self.n_q)[:-1]]).astype(int)
         table, total = synth.page_table(seed, self.n_kv, page_size)
         kp, vp = synth.to_paged(seqs, table, total, page_size)
@@ -103,6 +160,24 @@ def oracle_lists_for(db: DeviceBatch, masks, prm_kw):
     return O.expand_rescue(masks, db.n_q, db.n_kv, prm_kw["block"], prm_kw["tile"],
                            prm_kw["n_local"], prm_kw["n_sink"], prm_kw["eta"],
                            prm_kw["rho"], prm_kw["seed"])
+
+
+def head_mask_compare(gpu_head: np.ndarray, head_keep: np.ndarray, head_tie: np.ndarray,
+                      gpu_mask: np.ndarray = None):
+    """Per-query-head keep sets (eq18) against the oracle's: every cell that
+    is not a near-tie for its head must match; returns the near-tie cells
+    that differ.  Given the GPU's block mask, it must be the OR of the GPU's
+    own head sets over each GQA group, bit for bit."""
+    assert set(np.unique(gpu_head)) <= {0, 1}, "head mask holds values other than 0 / 1"
+    got = gpu_head.astype(bool)
+    bad = np.argwhere(~head_tie & (got != head_keep))
+    assert bad.size == 0, (f"per-head mismatches on {len(bad)} non-tie cells "
+                           f"(e.g. {bad[:5].tolist()})")
+    if gpu_mask is not None:
+        h_kv = gpu_mask.shape[0]
+        union = got.reshape(h_kv, -1, *got.shape[1:]).any(axis=1)
+        assert np.array_equal(union, gpu_mask.astype(bool)), "block mask != OR of head masks"
+    return int((head_tie & (got != head_keep)).sum())
 
 
 def mask_compare(gpu_mask: np.ndarray, oracle_mask: np.ndarray, status: np.ndarray):

@@ -28,8 +28,29 @@ def test_every_declared_symbol_is_exported():
         assert hasattr(lib, n), n
 
 
+def declared_parameters():
+    """Parameter lists of the declared entry points, as written in the header."""
+    text = re.sub(r"/\*.*?\*/", " ", open(HEADER).read(), flags=re.S)
+    out = {}
+    for name, params in re.findall(r"^(?:int|const char\*)\s+(bfla_\w+)\(([^)]*)\);", text,
+                                   re.M):
+        params = " ".join(params.split())
+        out[name] = [] if params in ("", "void") else [x.strip() for x in params.split(",")]
+    return out
+
+
+def test_binding_signatures_match_the_header():
+    decl = declared_parameters()
+    assert set(decl) == set(bfla.EXPORTS)
+    for name, params in decl.items():
+        assert len(params) == len(bfla._SIGS[name]), (name, params)
+    # the per-query-head keep sets (eq18) are an optional output of Stage 1
+    est = decl["bfla_estimate_mask"]
+    assert est[5] == "float* dbg_scores" and est[6] == "uint8_t* dbg_head_mask"
+
+
 def test_version_and_status_strings():
-    assert bfla.bfla_version() == "0.1.0"
+    assert bfla.bfla_version() == "0.2.0"
     assert bfla.bfla_status_string(0) == "ok"
     assert bfla.bfla_status_string(4) == "list capacity too small"
 
@@ -106,11 +127,11 @@ def test_entry_points_reject_before_launch():
     addr = C.c_void_p(1 << 20)
     # null block mask
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), None, None,
-                              addr, 1 << 30, None)
+                              None, addr, 1 << 30, None)
     assert st == bfla.BFLA_ERR_INVALID_ARG
     # workspace too small and no dbg output
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, None,
-                              addr, 4, None)
+                              None, addr, 4, None)
     assert st == bfla.BFLA_ERR_WORKSPACE
     # list capacity too small
     st = L.bfla_expand_rescue(C.byref(p.c), C.byref(prm), addr, addr, addr, 3, addr, 1 << 20,
@@ -180,7 +201,7 @@ def test_estimate_address_limits():
     # q rows of one score tile (128 groups of 64 tokens) spanning >= 2 GiB
     wide = bfla.bfla_view(1 << 20, None, 0, 64, 1 << 18)
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(wide), C.byref(kv), addr,
-                              addr, None, 0, None)
+                              addr, None, None, 0, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
     # paged K: 128 groups of 512 tokens cover 4097 16-token pages
     big = bfla.params(block=1024, group=512)
@@ -188,7 +209,7 @@ def test_estimate_address_limits():
                       1 << 20, 64)
     q = bfla.bfla_view(1 << 20, None, 0, 256 * 64, 64)
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(big), C.byref(q), C.byref(pk), addr, addr,
-                              None, 0, None)
+                              None, None, 0, None)
     assert st == bfla.BFLA_ERR_UNSUPPORTED
     assert "pages" in L.bfla_last_error().decode()
 

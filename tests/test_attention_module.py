@@ -25,3 +25,27 @@ def test_shape_rules():
     k = torch.empty(2, 4, 8, 64, dtype=torch.bfloat16, device="meta")
     with pytest.raises(ValueError):
         _layout(q, k, k)   # meta tensors are not on the GPU
+
+
+def test_v_with_other_strides_than_k_is_rejected():
+    # K a transposed view, V contiguous: same shape, different strides; the
+    # library would read V with K's strides, so the module refuses
+    q = _t(2, 4, 8, 64)
+    k = _t(2, 8, 2, 64).transpose(1, 2)
+    v = _t(2, 2, 8, 64)
+    assert k.shape == v.shape and k.stride() != v.stride()
+    with pytest.raises(ValueError, match="strides"):
+        BlockFilteredAttention()(q, k, v)
+
+
+def test_kv_descriptor_checks():
+    from paper_2605_12193_amd import bfla
+    k = _t(2, 8, 64)
+    with pytest.raises(ValueError, match="same shape and strides"):
+        bfla.KV(k, _t(8, 2, 64).transpose(0, 1))
+    pages = _t(4, 16, 2, 64)
+    for table in (torch.zeros(1, 4, dtype=torch.int64),
+                  torch.zeros(4, 2, dtype=torch.int32).t(),
+                  None):
+        with pytest.raises(ValueError, match="block_table"):
+            bfla.KV(pages, pages, paged=True, block_table=table)

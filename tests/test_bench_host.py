@@ -91,10 +91,7 @@ def test_committed_score_traffic_matches_the_score_kernel_source():
         assert t is not None and t > 0, f"{wl}: stale or unreadable score-kernel traffic"
 
 
-def test_sampled_mask_check_counts_sure_and_tie_mismatches():
-    # the bench's oracle leg compares the GPU block mask on the block rows it
-    # samples: fed the oracle's own mask it finds no mismatch; a flipped sure
-    # cell is counted as a sure mismatch
+def _tiny_oracle_pass():
     import numpy as np
     import torch
     from oracle import bfla_oracle as O
@@ -102,18 +99,53 @@ def test_sampled_mask_check_counts_sure_and_tie_mismatches():
     wl = synth.workload("tiny_2k")
     seqs = synth.make_inputs(wl)
     n = seqs[0].q.shape[1]
-    q, k = (t.double().numpy() for t in (seqs[0].q, seqs[0].k))
-    st = O.estimate_mask(q, k, wl.block, wl.group, wl.gamma, O.default_scale(wl.head_dim))
+    q, k, v = (t.double().numpy() for t in (seqs[0].q, seqs[0].k, seqs[0].v))
+    alpha = O.default_scale(wl.head_dim)
+    st = O.estimate_mask(q, k, wl.block, wl.group, wl.gamma, alpha)
+    rp, cols, _ = O.expand_rescue([st["mask"]], [n], [n], wl.block, wl.tile, wl.n_local,
+                                  wl.n_sink, wl.eta, wl.rho, wl.seed)
+    o, _ = O.attention(q, k, v, wl.tile, alpha, rp, cols)
 
     class Inp:
         pass
     inp = Inp()
     inp.seqs, inp.n = seqs, [n]
-    out = torch.zeros(wl.h_q, n, wl.head_dim, dtype=torch.bfloat16)
-    inp.out_rows = lambda o, r, p, t0, t1: o[p, t0:t1].float().numpy()
-    mask = st["mask"].reshape(-1).astype(np.uint8)
-    _, _, m = bench.cpu_baseline(wl, inp, out, 1.0, gpu_mask=mask)
-    assert m["block_rows"] > 0 and m["sure_mismatch"] == 0 and m["tie_mismatch"] == 0
-    bad = 1 - mask   # every cell flipped: every sampled sure cell now differs
-    _, _, m2 = bench.cpu_baseline(wl, inp, out, 1.0, gpu_mask=bad)
-    assert m2["sure_mismatch"] == m2["blocks"] - m2["tie_blocks"] > 0
+    inp.out_rows = lambda oo, r, p, t0, t1: oo[p, t0:t1].numpy()
+    return wl, inp, torch.from_numpy(o), st["mask"].reshape(-1).astype(np.uint8), rp, cols
+
+
+def test_cpu_baseline_checks_masks_lists_and_outputs():
+    # fed the oracle's own mask, lists and outputs as the "GPU" results, the
+    # bench's oracle leg finds no mismatch; a flipped mask is a sure mismatch
+    # on every sure cell, and a changed list is counted
+    import numpy as np
+    wl, inp, out, mask, rp, cols = _tiny_oracle_pass()
+    cpu, err, m, lst = bench.cpu_baseline(wl, inp, out, mask, rp, cols, rows=16)
+    assert m["cells"] == mask.size and m["sure_mismatch"] == 0 and m["tie_mismatch"] == 0
+    assert lst["rows"] == len(rp) - 1 and lst["rows_differ"] == 0
+    assert err["max_abs"] < 1e-12 and err["rows"] >= 16
+    assert cpu["kind"] == "oracle" and cpu["extrapolated"] and cpu["value"] > 0
+    assert cpu["attention_sample"]["of_kept_tiles"] == int(rp[-1])
+    assert cpu["cores"] >= 1 and cpu["nproc"] >= 1 and cpu["cpu_model"]
+    _, _, m2, _ = bench.cpu_baseline(wl, inp, out, 1 - mask, rp, cols, rows=4)
+    assert m2["sure_mismatch"] == m2["cells"] - m2["tie_cells"] > 0
+    cols2 = cols.copy()
+    cols2[0] += 1
+    _, _, _, lst2 = bench.cpu_baseline(wl, inp, out, mask, rp, cols2, rows=4)
+    assert lst2["rows_differ"] == 1
+
+
+def test_stratified_rows_cover_every_head_and_range():
+    import numpy as np
+    rng = np.random.default_rng(0)
+    rows = bench.stratified_rows([131072], 8, 64, 256, rng)
+    assert len(rows) == 256
+    for h in range(8):
+        qts = sorted(qt for r, hh, qt in rows if hh == h)
+        assert len(qts) == 32
+        # one q-tile in each of 32 equal ranges of the 2048 q-tiles
+        assert [qt // 64 for qt in qts] == list(range(32))
+    # a batch of requests of different lengths: every (request, head) pair
+    rows = bench.stratified_rows([300, 5000], 2, 64, 20, rng)
+    assert {(r, h) for r, h, _ in rows} == {(0, 0), (0, 1), (1, 0), (1, 1)}
+    assert all(0 <= qt < -(-[300, 5000][r] // 64) for r, _, qt in rows)

@@ -7,7 +7,8 @@ import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import DeviceBatch, compare_outputs, mask_compare, oracle_lists_for
+from parity_util import (DeviceBatch, GuardedBuffers, compare_outputs, head_mask_compare,
+                         mask_compare, oracle_lists_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -20,23 +21,33 @@ def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
     seqs = synth.make_inputs(wl, seqlens=seqlens)
     db = DeviceBatch(seqs, n_q)
     prm = bfla.params(**KW)
-    buf = bfla.Buffers(db.prob, prm)
-    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    buf = GuardedBuffers(db.prob, prm, head_mask=True)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
+                            dbg_head_mask=buf.head_mask)
+    torch.cuda.synchronize()
+    buf.check("estimate_mask")
     bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
     torch.cuda.synchronize()
+    buf.check("expand_rescue")
     rp_gpu = buf.row_ptr.cpu().numpy()
     assert rp_gpu[0] == 0 and np.all(np.diff(rp_gpu) >= 0) and rp_gpu[-1] <= buf.cols.numel()
     bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, buf.row_ptr, buf.cols, db.ov, buf.lse)
     torch.cuda.synchronize()
+    buf.check("sparse_prefill")
+    db.o_guard.check("sparse_prefill O")
     alpha = O.default_scale(c)
     gm_all = buf.block_mask.cpu().numpy()
-    masks, off = [], 0
+    gh_all = buf.head_mask.cpu().numpy()
+    masks, off, hoff = [], 0, 0
     for r in range(len(seqs)):
         q, k, _ = db.host(r)
         st = O.estimate_mask(q, k, KW["block"], KW["group"], KW["gamma"], alpha)
         gm = gm_all[off:off + st["mask"].size].reshape(st["mask"].shape)
+        gh = gh_all[hoff:hoff + st["scores"].size].reshape(st["scores"].shape)
         off += st["mask"].size
+        hoff += st["scores"].size
         mask_compare(gm, st["mask"], st["status"])
+        head_mask_compare(gh, st["head_keep"], st["head_tie"], gm)
         masks.append(gm)
     rp, cols, _ = oracle_lists_for(db, masks, KW)
     assert np.array_equal(rp_gpu, rp)
@@ -55,6 +66,7 @@ def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
     db.o.fill_(float("nan"))
     bfla.bfla_dense_prefill(db.prob, prm, db.qv, db.kv, db.ov)
     torch.cuda.synchronize()
+    db.o_guard.check("dense_prefill O")
     for r in range(len(seqs)):
         q, k, v = db.host(r)
         want, _ = O.attention(q, k, v, 64, alpha)

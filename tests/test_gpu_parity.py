@@ -11,8 +11,8 @@ import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import (DeviceBatch, compare_outputs, lists_to_device, mask_compare,
-                         oracle_lists_for)
+from parity_util import (DeviceBatch, Guarded, GuardedBuffers, compare_outputs,
+                         head_mask_compare, lists_to_device, mask_compare, oracle_lists_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -155,19 +155,22 @@ def test_estimate_mask_matches_oracle(shape, gamma):
     db = _make(*shape)
     kw, prm = _params(gamma=gamma)
     st = _oracle_stage1(db, kw)
-    buf = bfla.Buffers(db.prob, prm)
-    buf.block_mask.fill_(9)
-    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    buf = GuardedBuffers(db.prob, prm, head_mask=True)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
+                            dbg_head_mask=buf.head_mask)
     torch.cuda.synchronize()
+    buf.check("estimate_mask")
     got_mask = buf.block_mask.cpu().numpy()
     got_s = buf.scores.cpu().numpy()
+    got_h = buf.head_mask.cpu().numpy()
     alpha = O.default_scale(db.c)
     mo = so = 0
-    ties = 0
+    ties = head_ties = 0
     for r, s in enumerate(st):
         n_m, n_s = s["mask"].size, s["scores"].size
         gm = got_mask[mo:mo + n_m].reshape(s["mask"].shape)
         gs = got_s[so:so + n_s].reshape(s["scores"].shape)
+        gh = got_h[so:so + n_s].reshape(s["scores"].shape)
         mo += n_m
         so += n_s
         assert np.array_equal(np.isinf(gs), np.isinf(s["scores"]))
@@ -176,7 +179,28 @@ def test_estimate_mask_matches_oracle(shape, gamma):
         assert err.max() < 1e-4, f"alpha*S error {err.max():.2e}"
         assert set(np.unique(gm)) <= {0, 1}
         ties += mask_compare(gm, s["mask"], s["status"])
-    print(f"near-tie mismatches: {ties}")
+        head_ties += head_mask_compare(gh, s["head_keep"], s["head_tie"], gm)
+    print(f"near-tie mismatches: {ties} (per head: {head_ties})")
+
+
+def test_head_mask_is_optional_and_changes_nothing():
+    """The per-head output is a debug view: the block mask and scores are the
+    same bit for bit with and without it, and without dbg_scores the scores
+    go to the workspace."""
+    db = _make(*SHAPES[5])
+    kw, prm = _params()
+    a = GuardedBuffers(db.prob, prm, head_mask=True)
+    b = GuardedBuffers(db.prob, prm)
+    ws = Guarded(bfla.bfla_workspace_size(db.prob, prm, bfla.BFLA_WS_ESTIMATE), torch.uint8)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, a.block_mask, dbg_scores=a.scores,
+                            dbg_head_mask=a.head_mask)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, b.block_mask, workspace=ws.t)
+    torch.cuda.synchronize()
+    a.check("with head mask")
+    b.check("without")
+    ws.check("estimate workspace")
+    assert torch.equal(a.block_mask, b.block_mask)
+    assert torch.equal(a.scores.view(torch.int32), ws.t.view(torch.float32).view(torch.int32))
 
 
 @pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[2], SHAPES[4], SHAPES[8]],
@@ -184,13 +208,18 @@ def test_estimate_mask_matches_oracle(shape, gamma):
 def test_end_to_end_pipeline(shape):
     db = _make(*shape)
     kw, prm = _params()
-    buf = bfla.Buffers(db.prob, prm)
+    buf = GuardedBuffers(db.prob, prm)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    torch.cuda.synchronize()
+    buf.check("estimate_mask")
     bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
     torch.cuda.synchronize()
+    buf.check("expand_rescue")
     _host_check_lists(db, buf)
     bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, buf.row_ptr, buf.cols, db.ov, buf.lse)
     torch.cuda.synchronize()
+    buf.check("sparse_prefill")
+    db.o_guard.check("sparse_prefill O")
     # lists == oracle tile stage applied to the GPU's own block mask
     gm = buf.block_mask.cpu().numpy()
     masks, off = [], 0

@@ -13,7 +13,8 @@ import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import DeviceBatch, PagedBatch, compare_outputs, mask_compare
+from parity_util import (DeviceBatch, Guarded, GuardedBuffers, PagedBatch, compare_outputs,
+                         head_mask_compare, mask_compare)
 
 pytestmark = pytest.mark.gpu
 
@@ -57,30 +58,44 @@ def test_random_configuration_matches_oracle(case):
     seqs = synth.make_inputs(wl, seqlens=d["n_kv"])
     if d["paged"]:
         bt = PagedBatch(seqs, d["n_q"], d["page_size"], d["data_seed"])
-        od = torch.full_like(bt.o, float("nan"))
+        od_guard = Guarded(bt.o.numel(), bt.o.dtype, fill=float("nan"))
+        od = od_guard.t.view(bt.o.shape)
         odv = bfla.view_packed(od, bt.starts)
         dense_of = lambda r: od[bt.starts[r]:bt.starts[r] + bt.n_q[r]].transpose(0, 1).float().cpu().numpy()
     else:
         bt = DeviceBatch(seqs, d["n_q"])
-        od = torch.full_like(bt.o, float("nan"))
+        od_guard = Guarded(bt.o.numel(), bt.o.dtype, fill=float("nan"))
+        od = od_guard.t.view(bt.o.shape)
         odv = bfla.View(od, od.stride(0), od.stride(1),
                         batch_offsets=[int(s) * d["c"] for s in bt.q_start])
         dense_of = lambda r: od[:, bt.q_start[r]:bt.q_start[r] + bt.n_q[r]].float().cpu().numpy()
     kw = d["kw"]
     prm = bfla.params(**kw)
-    buf = bfla.Buffers(bt.prob, prm)
-    bfla.bfla_estimate_mask(bt.prob, prm, bt.qv, bt.kv, buf.block_mask, dbg_scores=buf.scores)
+    buf = GuardedBuffers(bt.prob, prm, head_mask=True)
+    bfla.bfla_estimate_mask(bt.prob, prm, bt.qv, bt.kv, buf.block_mask, dbg_scores=buf.scores,
+                            dbg_head_mask=buf.head_mask)
+    torch.cuda.synchronize()
+    buf.check("estimate_mask")
     bfla.bfla_expand_rescue(bt.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
     torch.cuda.synchronize()
+    buf.check("expand_rescue")
     rp = buf.row_ptr.cpu().numpy()
     assert rp[0] == 0 and np.all(np.diff(rp) >= 0) and rp[-1] <= buf.cols.numel()
     bfla.bfla_sparse_prefill(bt.prob, prm, bt.qv, bt.kv, buf.row_ptr, buf.cols, bt.ov, buf.lse)
-    dense_lse = torch.full_like(buf.lse, float("nan"))
+    torch.cuda.synchronize()
+    buf.check("sparse_prefill")
+    bt.o_guard.check("sparse_prefill O")
+    dense_lse_guard = Guarded(buf.lse.numel(), torch.float32, fill=float("nan"))
+    dense_lse = dense_lse_guard.t
     bfla.bfla_dense_prefill(bt.prob, prm, bt.qv, bt.kv, odv, dense_lse)
     torch.cuda.synchronize()
+    od_guard.check("dense_prefill O")
+    dense_lse_guard.check("dense_prefill lse")
 
     alpha = O.default_scale(d["c"])
     gm = buf.block_mask.cpu().numpy()
+    gh = buf.head_mask.cpu().numpy()
+    hoff = 0
     lse = buf.lse.cpu().numpy()
     dlse = dense_lse.cpu().numpy()
     masks, hosts, off = [], [], 0
@@ -95,6 +110,9 @@ def test_random_configuration_matches_oracle(case):
         off += d["h_kv"] * lq * lkv
         st = O.estimate_mask(q, k, kw["block"], kw["group"], kw["gamma"], alpha)
         ties += mask_compare(gmr, st["mask"], st["status"])
+        ghr = gh[hoff:hoff + st["scores"].size].reshape(st["scores"].shape)
+        hoff += st["scores"].size
+        ties += head_mask_compare(ghr, st["head_keep"], st["head_tie"], gmr)
         masks.append(gmr)
     want_rp, want_cols, _ = O.expand_rescue(masks, d["n_q"], d["n_kv"], kw["block"], 64,
                                             kw["n_local"], kw["n_sink"], kw["eta"], kw["rho"],

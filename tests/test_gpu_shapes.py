@@ -12,7 +12,7 @@ import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import (DeviceBatch, PagedBatch, compare_outputs, lists_to_device,
+from parity_util import (DeviceBatch, Guarded, PagedBatch, compare_outputs, lists_to_device,
                          oracle_lists_for)
 
 pytestmark = pytest.mark.gpu
@@ -45,9 +45,12 @@ def test_sparse_shape(c, m):
     st = O.estimate_mask(q, k, kw["block"], kw["group"], kw["gamma"], O.default_scale(c))
     rp, cols, _ = oracle_lists_for(db, [st["mask"]], kw)
     drp, dcols = lists_to_device(rp, cols)
-    lse = torch.full((m * N,), float("nan"), device="cuda")
+    lg = Guarded(m * N, torch.float32, fill=float("nan"))
+    lse = lg.t
     bfla.bfla_sparse_prefill(db.prob, prm, db.qv, db.kv, drp, dcols, db.ov, lse)
     torch.cuda.synchronize()
+    lg.check("sparse lse")
+    db.o_guard.check("sparse O")
     want, want_lse = O.attention(q, k, v, 64, O.default_scale(c), rp, cols, 0)
     compare_outputs(db.o_of(0), want, f"sparse C={c} m={m}")
     _check_lse(lse.cpu().numpy(), want_lse)
@@ -57,9 +60,12 @@ def test_sparse_shape(c, m):
 def test_dense_shape(c, m):
     db = _batch(c, m)
     _, prm = _params()
-    lse = torch.full((m * N,), float("nan"), device="cuda")
+    lg = Guarded(m * N, torch.float32, fill=float("nan"))
+    lse = lg.t
     bfla.bfla_dense_prefill(db.prob, prm, db.qv, db.kv, db.ov, lse)
     torch.cuda.synchronize()
+    lg.check("dense lse")
+    db.o_guard.check("dense O")
     q, k, v = db.host(0)
     want, want_lse = O.attention(q, k, v, 64, O.default_scale(c))
     compare_outputs(db.o_of(0), want, f"dense C={c} m={m}")
@@ -98,15 +104,20 @@ def _paged_case(c, m, page_size):
     rp, cols, _ = O.expand_rescue([masks], [N], [N], kw["block"], kw["tile"], kw["n_local"],
                                   kw["n_sink"], kw["eta"], kw["rho"], kw["seed"])
     drp, dcols = lists_to_device(rp, cols)
-    lse = torch.full((2 * m * N,), float("nan"), device="cuda")
+    lg = Guarded(2 * m * N, torch.float32, fill=float("nan"))
+    lse = lg.t
     bfla.bfla_sparse_prefill(pb.prob, prm, pb.qv, pb.kv, drp, dcols, pb.ov, lse)
     torch.cuda.synchronize()
+    lg.check("paged sparse lse")
+    pb.o_guard.check("paged sparse O")
     want, want_lse = O.attention(q, k, v, 64, alpha, rp, cols, 0)
     compare_outputs(pb.o_of(0), want, f"paged sparse C={c} m={m}")
     _check_lse(lse.cpu().numpy(), want_lse)
     lse.fill_(float("nan"))
     bfla.bfla_dense_prefill(pb.prob, prm, pb.qv, pb.kv, pb.ov, lse)
     torch.cuda.synchronize()
+    lg.check("paged dense lse")
+    pb.o_guard.check("paged dense O")
     want, want_lse = O.attention(q, k, v, 64, alpha)
     compare_outputs(pb.o_of(0), want, f"paged dense C={c} m={m}")
     _check_lse(lse.cpu().numpy(), want_lse)
