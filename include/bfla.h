@@ -216,6 +216,28 @@ int bfla_expand_rescue(const bfla_problem* prob, const bfla_params* params,
                        int32_t* cols, size_t cols_capacity, void* workspace,
                        size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * bfla_expand_rescue with its workspace (per-row counts and keep ballots)
+ * taken from a fixed scratch buffer that the library holds on each GPU it
+ * runs on until the process ends, BFLA_EXPAND_SCRATCH_BYTES large; nothing
+ * is allocated.  Same arguments, outputs and errors as bfla_expand_rescue
+ * without the workspace; a problem whose workspace would exceed the scratch
+ * (bfla_workspace_size(BFLA_WS_EXPAND) > BFLA_EXPAND_SCRATCH_BYTES) is
+ * rejected with BFLA_ERR_WORKSPACE before anything is enqueued.
+ *   stream  must belong to the current device (its scratch is used).
+ * The scratch of a device is shared by every call on it and keeps the last
+ * call's contents (nothing in it needs clearing: every call writes each
+ * word it reads); calls that overlap on one GPU (different streams, or
+ * threads without ordering between them) race on it and must be serialised
+ * by the caller.  The first call on a device looks the buffer up
+ * (hipGetSymbolAddress); make that call outside graph capture.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, CAPACITY, HIP. */
+#define BFLA_EXPAND_SCRATCH_BYTES (16u << 20)
+int bfla_expand_rescue_noalloc(const bfla_problem* prob, const bfla_params* params,
+                               const uint8_t* block_mask, int32_t* row_ptr,
+                               int32_t* cols, size_t cols_capacity, void* stream);
+
 /* Final sparse attention, eq27: for every query head p and query t (absolute
  * position N_c + t) of every request, softmax(scale * q.k) over the keys k
  * with k <= N_c + t whose tile is in the list of (request, floor(p/m),

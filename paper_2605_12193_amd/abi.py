@@ -12,6 +12,7 @@ BFLA_ERR_WORKSPACE, BFLA_ERR_CAPACITY, BFLA_ERR_HIP = 3, 4, 5
 BFLA_KV_CONTIGUOUS, BFLA_KV_PAGED = 0, 1
 BFLA_WS_ESTIMATE, BFLA_WS_EXPAND = 1, 2
 MAX_BATCH = 32
+EXPAND_SCRATCH_BYTES = 16 << 20
 
 
 class bfla_problem(C.Structure):
@@ -54,6 +55,9 @@ SIGS = {
     "bfla_expand_rescue": [C.POINTER(bfla_problem), C.POINTER(bfla_params), C.c_void_p,
                            C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p, C.c_size_t,
                            C.c_void_p],
+    "bfla_expand_rescue_noalloc": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
+                                   C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                   C.c_void_p],
     "bfla_sparse_prefill": [C.POINTER(bfla_problem), C.POINTER(bfla_params),
                             C.POINTER(bfla_view), C.POINTER(bfla_kv), C.c_void_p,
                             C.c_void_p, C.POINTER(bfla_view), C.c_void_p, C.c_void_p],

@@ -17,7 +17,8 @@ import torch
 
 from .abi import (BFLA_ERR_CAPACITY, BFLA_ERR_HIP, BFLA_ERR_INVALID_ARG,  # noqa: F401
                   BFLA_ERR_UNSUPPORTED, BFLA_ERR_WORKSPACE, BFLA_KV_CONTIGUOUS, BFLA_KV_PAGED,
-                  BFLA_OK, BFLA_WS_ESTIMATE, BFLA_WS_EXPAND, EXPORTS, MAX_BATCH, bfla_kv,
+                  BFLA_OK, BFLA_WS_ESTIMATE, BFLA_WS_EXPAND, EXPAND_SCRATCH_BYTES, EXPORTS,
+                  MAX_BATCH, bfla_kv,
                   bfla_params, bfla_problem, bfla_view)
 from .abi import SIGS as _SIGS  # noqa: F401
 from .abi import bind as _bind
@@ -195,6 +196,15 @@ def bfla_expand_rescue(prob: Problem, prm: bfla_params, block_mask: torch.Tensor
                                     _ptr(row_ptr), _ptr(cols), cols.numel(), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(),
                                     _stream(stream)))
+
+
+def bfla_expand_rescue_noalloc(prob: Problem, prm: bfla_params, block_mask: torch.Tensor,
+                               row_ptr: torch.Tensor, cols: torch.Tensor, stream=None) -> None:
+    """bfla_expand_rescue with the library's fixed per-device scratch in place of
+    a workspace (no allocation anywhere)."""
+    _check(lib().bfla_expand_rescue_noalloc(C.byref(prob.c), C.byref(prm), _ptr(block_mask),
+                                            _ptr(row_ptr), _ptr(cols), cols.numel(),
+                                            _stream(stream)))
 
 
 def bfla_sparse_prefill(prob: Problem, prm: bfla_params, q: View, kv: KV,

@@ -286,6 +286,54 @@ int prefill_common(const bfla_problem* prob, const bfla_params* pr, const bfla_v
   return BFLA_OK;
 }
 
+int expand_common(const bfla_problem* prob, const bfla_params* params,
+                  const uint8_t* block_mask, int32_t* row_ptr, int32_t* cols,
+                  size_t cols_capacity, void* workspace, size_t ws_bytes, bool use_scratch,
+                  void* stream) {
+  int st;
+  if ((st = check_problem(prob, params))) return st;
+  if (!block_mask || !row_ptr || !cols)
+    return fail(BFLA_ERR_INVALID_ARG, "block_mask / row_ptr / cols is NULL");
+  Sizes s = sizes_of(prob, params);
+  if ((st = check_rows_fit(s))) return st;
+  if (cols_capacity < (size_t)s.max_cols)
+    return fail(BFLA_ERR_CAPACITY, "cols capacity %zu < %lld causal tiles", cols_capacity,
+                (long long)s.max_cols);
+  size_t need = expand_workspace_bytes(s.n_rows, s.max_t_kv);
+  if (use_scratch) {
+    if (need > (size_t)BFLA_EXPAND_SCRATCH_BYTES)
+      return fail(BFLA_ERR_WORKSPACE,
+                  "tile stage needs %zu bytes of workspace, more than the %zu-byte scratch "
+                  "of bfla_expand_rescue_noalloc", need, (size_t)BFLA_EXPAND_SCRATCH_BYTES);
+    hipError_t e = expand_scratch(&workspace);
+    if (e != hipSuccess) return hip_status(e, "expand_rescue_noalloc scratch lookup");
+    ws_bytes = BFLA_EXPAND_SCRATCH_BYTES;
+  }
+  if (!workspace || ws_bytes < need)
+    return fail(BFLA_ERR_WORKSPACE, "expand workspace %zu < %zu bytes", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 7)
+    return fail(BFLA_ERR_INVALID_ARG, "expand workspace not 8-byte aligned");
+  ExpandLaunch L{};
+  L.block_mask = block_mask;
+  L.row_ptr = row_ptr;
+  L.cols = cols;
+  L.counts = static_cast<int32_t*>(workspace);
+  L.partial = L.counts + ((s.n_rows + 63) / 64) * 64;
+  L.words_per_row = (int32_t)((s.max_t_kv + 63) / 64);
+  L.bits = reinterpret_cast<uint64_t*>(L.partial + 64);
+  L.n_rows = (int32_t)s.n_rows;
+  L.h_kv = prob->h_kv;
+  L.rb = params->block / params->tile;
+  L.n_local = params->n_local;
+  L.n_sink = params->n_sink;
+  L.eta = params->eta;
+  L.rho24 = (uint32_t)floor(params->rho * 16777216.0);
+  L.seed = params->seed;
+  L.batch = make_batch(prob, params, nullptr, nullptr, nullptr);
+  return hip_status(launch_expand(L, static_cast<hipStream_t>(stream)),
+                    use_scratch ? "expand_rescue_noalloc" : "expand_rescue");
+}
+
 }  // namespace
 
 extern "C" {
@@ -389,38 +437,15 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
 int bfla_expand_rescue(const bfla_problem* prob, const bfla_params* params,
                        const uint8_t* block_mask, int32_t* row_ptr, int32_t* cols,
                        size_t cols_capacity, void* workspace, size_t ws_bytes, void* stream) {
-  int st;
-  if ((st = check_problem(prob, params))) return st;
-  if (!block_mask || !row_ptr || !cols)
-    return fail(BFLA_ERR_INVALID_ARG, "block_mask / row_ptr / cols is NULL");
-  Sizes s = sizes_of(prob, params);
-  if ((st = check_rows_fit(s))) return st;
-  if (cols_capacity < (size_t)s.max_cols)
-    return fail(BFLA_ERR_CAPACITY, "cols capacity %zu < %lld causal tiles", cols_capacity,
-                (long long)s.max_cols);
-  size_t need = expand_workspace_bytes(s.n_rows, s.max_t_kv);
-  if (!workspace || ws_bytes < need)
-    return fail(BFLA_ERR_WORKSPACE, "expand workspace %zu < %zu bytes", ws_bytes, need);
-  if (reinterpret_cast<uintptr_t>(workspace) & 7)
-    return fail(BFLA_ERR_INVALID_ARG, "expand workspace not 8-byte aligned");
-  ExpandLaunch L{};
-  L.block_mask = block_mask;
-  L.row_ptr = row_ptr;
-  L.cols = cols;
-  L.counts = static_cast<int32_t*>(workspace);
-  L.partial = L.counts + ((s.n_rows + 63) / 64) * 64;
-  L.words_per_row = (int32_t)((s.max_t_kv + 63) / 64);
-  L.bits = reinterpret_cast<uint64_t*>(L.partial + 64);
-  L.n_rows = (int32_t)s.n_rows;
-  L.h_kv = prob->h_kv;
-  L.rb = params->block / params->tile;
-  L.n_local = params->n_local;
-  L.n_sink = params->n_sink;
-  L.eta = params->eta;
-  L.rho24 = (uint32_t)floor(params->rho * 16777216.0);
-  L.seed = params->seed;
-  L.batch = make_batch(prob, params, nullptr, nullptr, nullptr);
-  return hip_status(launch_expand(L, static_cast<hipStream_t>(stream)), "expand_rescue");
+  return expand_common(prob, params, block_mask, row_ptr, cols, cols_capacity, workspace,
+                       ws_bytes, false, stream);
+}
+
+int bfla_expand_rescue_noalloc(const bfla_problem* prob, const bfla_params* params,
+                               const uint8_t* block_mask, int32_t* row_ptr, int32_t* cols,
+                               size_t cols_capacity, void* stream) {
+  return expand_common(prob, params, block_mask, row_ptr, cols, cols_capacity, nullptr, 0,
+                       true, stream);
 }
 
 int bfla_sparse_prefill(const bfla_problem* prob, const bfla_params* params, const bfla_view* q,

@@ -51,6 +51,9 @@ struct ExpandLaunch {
 };
 
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream);
+// The current device's fixed tile-stage scratch (BFLA_EXPAND_SCRATCH_BYTES),
+// looked up once per device.
+hipError_t expand_scratch(void** ptr);
 size_t expand_workspace_bytes(int64_t n_rows, int64_t max_t_kv);
 
 struct EstimateLaunch {

@@ -11,8 +11,16 @@
 // the row counts; pass 2 is an exclusive scan of the counts in one
 // workgroup; pass 3 reads the ballots back and writes each kept tile at its
 // list position, so every keep / drop decision is taken once.
+#include <atomic>
+
 #include "bfla_device.h"
 #include "bfla_internal.h"
+
+// Workspace of bfla_expand_rescue_noalloc: one copy per device, for the life
+// of the process.  Host code never passes `scratch` itself to a kernel (on
+// the host it names a stand-in, not device memory): expand_scratch() looks up
+// each device's address once and every launch uses that.
+static __device__ __align__(256) uint8_t scratch[BFLA_EXPAND_SCRATCH_BYTES];
 
 namespace bfla {
 namespace {
@@ -155,6 +163,30 @@ __global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a)
 }
 
 }  // namespace
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::atomic<uintptr_t> g_scratch[kMaxDevices];  // device address, 0 = not looked up yet
+}  // namespace
+
+hipError_t expand_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  uintptr_t p = g_scratch[dev].load(std::memory_order_acquire);
+  if (p == 0) {
+    // with this device current: its own copy of the array
+    void* addr = nullptr;
+    e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (addr == nullptr) return hipErrorInvalidSymbol;
+    p = reinterpret_cast<uintptr_t>(addr);
+    g_scratch[dev].store(p, std::memory_order_release);
+  }
+  *ptr = reinterpret_cast<void*>(p);
+  return hipSuccess;
+}
 
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
   if (L.n_rows == 0) return hipSuccess;

@@ -135,6 +135,12 @@ def random_case(rng, L):
     st = L.bfla_expand_rescue(C.byref(p), C.byref(prm), a, a, a, max_cols, a, ws_exp, None)
     assert st in (OK, INVALID, UNSUP), st
     n_ok += st == OK
+    st = L.bfla_expand_rescue_noalloc(C.byref(p), C.byref(prm), a, a, a, max_cols, None)
+    assert st in (OK, INVALID, UNSUP, WS), st
+    # accepted only when its workspace fits the scratch; too large -> WORKSPACE
+    # (unless an earlier check already refused the problem)
+    assert st != OK or ws_exp <= abi.EXPAND_SCRATCH_BYTES, (st, ws_exp)
+    assert st != WS or ws_exp > abi.EXPAND_SCRATCH_BYTES, (st, ws_exp)
     st = L.bfla_sparse_prefill(C.byref(p), C.byref(prm), C.byref(q), C.byref(kv), a, a,
                                C.byref(q), a, None)
     assert st in (OK, INVALID, UNSUP), st

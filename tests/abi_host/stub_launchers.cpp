@@ -69,6 +69,12 @@ hipError_t launch_expand(const ExpandLaunch& L, hipStream_t) {
   return hipSuccess;
 }
 
+hipError_t expand_scratch(void** ptr) {
+  // a fake, aligned device address: the stub launchers never dereference it
+  *ptr = reinterpret_cast<void*>(uintptr_t(1) << 32);
+  return hipSuccess;
+}
+
 hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t) {
   ++g_launches[2];
   check_batch(L.batch, L.block);

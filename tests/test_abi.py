@@ -224,3 +224,31 @@ def test_expand_workspace_holds_counts_and_ballots():
         words = -(-max(-(-n // 64) for n in n_kv) // 64)
         want = (-(-cap.n_rows // 64) * 64 + 64) * 4 + cap.n_rows * words * 8
         assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) == want
+
+
+def test_noalloc_tile_stage_rejects_problems_beyond_its_scratch():
+    # the workspace of 8 KV heads x 4096 q-tiles x 64 ballot words is 16 MiB
+    # plus the row counts: one row past the fixed scratch; rejected before any
+    # device call (no GPU is touched here)
+    L = bfla.lib()
+    prm = bfla.params()
+    big = bfla.Problem([262144], [262144], 8, 8, 128)
+    need = bfla.bfla_workspace_size(big, prm, bfla.BFLA_WS_EXPAND)
+    assert need > bfla.EXPAND_SCRATCH_BYTES
+    cap = bfla.bfla_list_capacity(big, prm)
+    addr = C.c_void_p(1 << 20)
+    st = L.bfla_expand_rescue_noalloc(C.byref(big.c), C.byref(prm), addr, addr, addr,
+                                      cap.max_cols, None)
+    assert st == bfla.BFLA_ERR_WORKSPACE
+    assert b"scratch" in L.bfla_last_error()
+    # the other argument checks come first, as in bfla_expand_rescue
+    st = L.bfla_expand_rescue_noalloc(C.byref(big.c), C.byref(prm), addr, addr, addr, 3, None)
+    assert st == bfla.BFLA_ERR_CAPACITY
+    st = L.bfla_expand_rescue_noalloc(C.byref(big.c), C.byref(prm), None, addr, addr,
+                                      cap.max_cols, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG
+    # the largest workloads here fit: 128K x 8 KV heads, and the 4-request
+    # paged batch of 16K-128K tokens
+    for n in ([131072], [16384, 32768, 65536, 131072]):
+        p = bfla.Problem(n, n, 40, 8, 128)
+        assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) <= bfla.EXPAND_SCRATCH_BYTES
