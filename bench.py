@@ -358,7 +358,8 @@ class Runner:
         if marks:
             marks[0].record(self.stream)
         bfla.bfla_estimate_mask(inp.prob, prm, inp.qv, inp.kv, buf.block_mask,
-                                dbg_scores=buf.scores)
+                                dbg_scores=buf.scores,
+    workspace=buf.ws_estimate)
         if marks:
             marks[1].record(self.stream)
         bfla.bfla_expand_rescue(inp.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
@@ -375,7 +376,8 @@ class Runner:
         any prefill reads them."""
         bfla, inp, wl = self.bfla, self.inp, self.wl
         bfla.bfla_estimate_mask(inp.prob, prm, inp.qv, inp.kv, buf.block_mask,
-                                dbg_scores=buf.scores)
+                                dbg_scores=buf.scores,
+    workspace=buf.ws_estimate)
         bfla.bfla_expand_rescue(inp.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
                                 buf.ws_expand)
         self.torch.cuda.synchronize()

@@ -157,7 +157,10 @@ typedef struct bfla_params {
 
 enum { BFLA_WS_ESTIMATE = 1, BFLA_WS_EXPAND = 2 };
 
-/* Bytes of device workspace the call `which` needs (0 is possible). */
+/* Bytes of device workspace the call `which` needs (0 is possible): for
+ * BFLA_WS_ESTIMATE the split score GEMM's partial sums plus the block
+ * scores (enough with or without dbg_scores); for BFLA_WS_EXPAND the row
+ * counts and keep ballots of the tile stage. */
 int bfla_workspace_size(const bfla_problem* prob, const bfla_params* params,
                         int which, size_t* bytes);
 
@@ -182,8 +185,15 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
  *   dbg_scores     out, device float or NULL (then the workspace holds them).
  *   dbg_head_mask  out, device uint8 or NULL: the per-query-head keep sets
  *                  of eq18 that the union combines (layout above).
- *   workspace      device scratch of >= bfla_workspace_size(BFLA_WS_ESTIMATE)
- *                  (unused, and may be NULL, when dbg_scores is given).
+ *   workspace      device scratch, 256-byte aligned, of
+ *                  bfla_workspace_size(BFLA_WS_ESTIMATE) bytes: it holds the
+ *                  partial sums of the score GEMM when the problem has too
+ *                  few score tiles to fill the GPU and the GEMM's inner
+ *                  dimension is split (added in a fixed order, so results
+ *                  stay bit-identical run to run), then the block scores
+ *                  when dbg_scores is NULL.  With dbg_scores given, only the
+ *                  partial sums are needed (NULL / 0 is enough when there
+ *                  are none).
  * Errors: INVALID_ARG, UNSUPPORTED (also: m > 8; more than 65536 KV blocks
  * per request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
  * i.e. (128 g - 1) * stride_tok + head_dim >= 2^30; paged K where 128 g

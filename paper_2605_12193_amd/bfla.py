@@ -237,6 +237,8 @@ class Buffers:
         self.cols = torch.empty(max(cap.max_cols, 1), dtype=torch.int32, device=device)
         ws = bfla_workspace_size(prob, prm, BFLA_WS_EXPAND)
         self.ws_expand = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
+        ws = bfla_workspace_size(prob, prm, BFLA_WS_ESTIMATE)
+        self.ws_estimate = torch.empty(max(ws, 16), dtype=torch.uint8, device=device)
         n_lse = sum(prob.c.h_q * n for n in prob.n_q)
         self.lse = torch.empty(n_lse, dtype=torch.float32, device=device) if lse else None
 
@@ -244,7 +246,8 @@ class Buffers:
 def sparse_pass(prob: Problem, prm: bfla_params, q: View, kv: KV, o: View, buf: Buffers,
                 stream=None) -> None:
     """Stage 1 -> tile lists -> sparse prefill, all enqueued on one stream."""
-    bfla_estimate_mask(prob, prm, q, kv, buf.block_mask, dbg_scores=buf.scores, stream=stream)
+    bfla_estimate_mask(prob, prm, q, kv, buf.block_mask, dbg_scores=buf.scores,
+                       workspace=buf.ws_estimate, stream=stream)
     bfla_expand_rescue(prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand,
                        stream=stream)
     bfla_sparse_prefill(prob, prm, q, kv, buf.row_ptr, buf.cols, o, buf.lse, stream=stream)

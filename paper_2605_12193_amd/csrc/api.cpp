@@ -286,6 +286,12 @@ int prefill_common(const bfla_problem* prob, const bfla_params* pr, const bfla_v
   return BFLA_OK;
 }
 
+// Stage-1 workspace: the partial sums of a split score GEMM first, then the
+// block scores when the caller passes no dbg_scores.
+size_t estimate_ws_scores_offset(const EstimatePlan& plan) {
+  return (plan.partial_bytes + 255) / 256 * 256;
+}
+
 int expand_common(const bfla_problem* prob, const bfla_params* params,
                   const uint8_t* block_mask, int32_t* row_ptr, int32_t* cols,
                   size_t cols_capacity, void* workspace, size_t ws_bytes, bool use_scratch,
@@ -373,7 +379,12 @@ int bfla_workspace_size(const bfla_problem* prob, const bfla_params* params, int
   if (!bytes) return fail(BFLA_ERR_INVALID_ARG, "bytes is NULL");
   Sizes s = sizes_of(prob, params);
   if (which == BFLA_WS_ESTIMATE) {
-    *bytes = (size_t)s.score_elems * sizeof(float);
+    if (!estimate_supported(prob->head_dim, params->block, params->group))
+      return fail(BFLA_ERR_UNSUPPORTED, "block %d / group %d not built for head_dim %d",
+                  params->block, params->group, prob->head_dim);
+    const EstimatePlan plan = estimate_plan(prob->n_q, prob->n_kv, prob->batch, prob->h_q,
+                                            prob->head_dim, params->block, params->group);
+    *bytes = estimate_ws_scores_offset(plan) + (size_t)s.score_elems * sizeof(float);
   } else if (which == BFLA_WS_EXPAND) {
     *bytes = expand_workspace_bytes(s.n_rows, s.max_t_kv);
   } else {
@@ -408,13 +419,16 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
       return fail(BFLA_ERR_UNSUPPORTED, "request %d: more than %d KV blocks", r,
                   (int)kMaxBlocksPerRow);
   Sizes s = sizes_of(prob, params);
-  float* scores = dbg_scores;
-  if (!scores) {
-    size_t need = (size_t)s.score_elems * sizeof(float);
-    if (!workspace || ws_bytes < need)
-      return fail(BFLA_ERR_WORKSPACE, "estimate workspace %zu < %zu bytes", ws_bytes, need);
-    scores = static_cast<float*>(workspace);
-  }
+  const EstimatePlan plan = estimate_plan(prob->n_q, prob->n_kv, prob->batch, prob->h_q,
+                                          prob->head_dim, params->block, params->group);
+  const size_t off = estimate_ws_scores_offset(plan);
+  const size_t need = dbg_scores ? plan.partial_bytes : off + (size_t)s.score_elems * sizeof(float);
+  if (need > 0 && (!workspace || ws_bytes < need))
+    return fail(BFLA_ERR_WORKSPACE, "estimate workspace %zu < %zu bytes", ws_bytes, need);
+  if (need > 0 && (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return fail(BFLA_ERR_INVALID_ARG, "estimate workspace not 256-byte aligned");
+  float* scores = dbg_scores ? dbg_scores
+                             : reinterpret_cast<float*>(static_cast<char*>(workspace) + off);
   EstimateLaunch L{};
   L.q = q->data;
   L.q_sh = q->stride_head;
@@ -422,6 +436,8 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   L.kv = kv_addr(kv);
   L.block_mask = block_mask;
   L.scores = scores;
+  L.partials = plan.split > 1 ? static_cast<float*>(workspace) : nullptr;
+  L.split = plan.split;
   L.head_mask = dbg_head_mask;
   L.h_q = prob->h_q;
   L.h_kv = prob->h_kv;

@@ -16,6 +16,24 @@ constexpr int kScoreTileM = 256;
 constexpr int kScoreTileN = 128;
 constexpr int kScoreChunk = 64;
 constexpr int kScorePagesMax = 2048;
+// stages per inner accumulation chain of the score GEMM (summed into a
+// second accumulator; a split of the inner dimension cuts between chains)
+constexpr int kScoreChain = 8;
+
+// How Stage 1 runs a problem: score tiles in the launch (all, and those
+// holding a causal block pair), the split of the inner dimension (1: none;
+// S > 1: S workgroups per tile, each a run of whole chains, whose raw group
+// sums a second kernel adds in a fixed order before the max pool), and the
+// workspace bytes those partial sums take.  A function of the problem only,
+// so results do not depend on the device.
+struct EstimatePlan {
+  int32_t split;
+  int64_t total_tiles;
+  int64_t causal_tiles;
+  size_t partial_bytes;
+};
+EstimatePlan estimate_plan(const int32_t* n_q, const int32_t* n_kv, int batch, int h_q,
+                           int head_dim, int block, int group);
 
 struct PrefillLaunch {
   const void* q;
@@ -62,6 +80,8 @@ struct EstimateLaunch {
   KvAddr kv;
   uint8_t* block_mask;
   float* scores;      // [per request H_q x L_q x L_kv], workspace or dbg output
+  float* partials;    // split > 1: [split][tiles][kScoreTileM][kScoreTileN] raw group sums
+  int32_t split;
   uint8_t* head_mask; // [per request H_q x L_q x L_kv] per-head keep sets, or null
   int32_t h_q, h_kv, head_dim;
   int32_t block, group;

@@ -14,6 +14,10 @@
 // and stores it as float.  Accumulation is two-level: chains of 32 MFMA
 // steps (512 products) are summed into a second float accumulator, which
 // keeps the score error well inside the near-tie band of the selection.
+// When a problem has too few tiles to fill the chip (a split S > 1 from
+// estimate_plan), each tile runs as S workgroups over consecutive runs of
+// whole chains that store their raw group sums; pool_kernel adds the S sums
+// in part order, then pools and stores as the epilogue would.
 //
 // Kernel 2 (select): one workgroup per (request, KV head, query block),
 // one wave per query head of the group: block softmax over the causal KV
@@ -36,7 +40,7 @@ constexpr int BK = kScoreChunk;   // inner elements per stage
 constexpr int NW = 8;
 constexpr int NT = 64 * NW;
 constexpr int XB = BM / NW / 32;   // 32-row MFMA blocks per wave
-constexpr int CHAIN = 8;    // stages per inner accumulation chain (32 MFMA k-steps)
+constexpr int CHAIN = kScoreChain;  // stages per inner accumulation chain (32 MFMA k-steps)
 constexpr int MAX_LKV = 65536;
 
 struct ScoreArgs {
@@ -44,9 +48,13 @@ struct ScoreArgs {
   int64_t q_sh, q_st;
   KvAddr kv;
   float* scores;
+  float* partials;   // split > 1: raw group sums [split][tiles][BM][BN]
   int32_t h_q, h_kv, m;
   int32_t C, g, b, G;
   int32_t gc;        // g * C
+  int32_t split;     // workgroups per tile, each part_stages stages
+  int32_t part_stages;
+  int32_t total_tiles;
   Batch batch;       // work_begin = first tile of request r
 };
 
@@ -125,13 +133,16 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hi = lane >> 5;
 
-  // ---- tile decode: (request, tile rank, head) with the KV head fastest ----
-  const int ri = find_req(a.batch, blockIdx.x);
+  // ---- tile decode: (split part, request, tile rank, head) with the KV
+  // head fastest and the part slowest ----
+  const int part = blockIdx.x / a.total_tiles;
+  const int tile_id = blockIdx.x - part * a.total_tiles;
+  const int ri = find_req(a.batch, tile_id);
   const ReqDesc& R = a.batch.r[ri];
   const int n_q = R.n_q, n_kv = R.n_kv;
   const int64_t q_off = R.q_off, kv_off = R.kv_off;
   const int bt_row = R.bt_row;
-  const int local = blockIdx.x - R.work_begin;
+  const int local = tile_id - R.work_begin;
   const int nqg = (n_q + a.g - 1) / a.g;    // query groups
   const int nkg = (n_kv + a.g - 1) / a.g;   // key groups
   const int ntj = col_tiles(nkg);
@@ -240,7 +251,9 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) { acc[x][y][r] = 0.f; tot[x][y][r] = 0.f; }
 
-  const int n_stage = a.gc / BK;
+  // this workgroup's stages: a run of whole chains
+  const int st_begin = part * a.part_stages;
+  const int st_end = st_begin + a.part_stages;
   auto compute = [&](const bf16_t* A, const bf16_t* B) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
@@ -265,21 +278,21 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
   constexpr int VM_AHEAD = 0x0F70 | VM_STAGE, VM0 = 0x0F70;
   static_assert(NSTAGE == 3 && VM_STAGE < 16, "one stage ahead, vmcnt below 16");
 
-  // prologue: stages 0 .. NSTAGE - 2 in flight
-  for (int st = 0; st < NSTAGE - 1 && st < n_stage; ++st) issue(st);
-  for (int c0 = 0; c0 < n_stage; c0 += CHAIN) {
-    const int c1 = min(c0 + CHAIN, n_stage);
+  // prologue: stages st_begin .. st_begin + NSTAGE - 2 in flight
+  for (int st = st_begin; st < st_begin + NSTAGE - 1 && st < st_end; ++st) issue(st);
+  for (int c0 = st_begin; c0 < st_end; c0 += CHAIN) {
+    const int c1 = min(c0 + CHAIN, st_end);
     for (int st = c0; st < c1; ++st) {
       // this wave's loads of stage st are done once at most the loads of the
       // stage after it (VM_STAGE) remain; the barrier then makes every wave's
       // part visible, and also tells that every wave is done reading the slot
       // refilled next (stage st - 1's)
-      if (st + 1 < n_stage) __builtin_amdgcn_s_waitcnt(VM_AHEAD);
+      if (st + 1 < st_end) __builtin_amdgcn_s_waitcnt(VM_AHEAD);
       else __builtin_amdgcn_s_waitcnt(VM0);
       // plain barrier: a __syncthreads() fence would also wait for the
       // loads still in flight for the later stages
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-      if (st + NSTAGE - 1 < n_stage) issue(st + NSTAGE - 1);
+      if (st + NSTAGE - 1 < st_end) issue(st + NSTAGE - 1);
       const int slot = st % NSTAGE;
       compute(&ring[slot][0], &ring[slot][A_ELEMS]);
     }
@@ -292,8 +305,23 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
         for (int r = 0; r < 16; ++r) { tot[x][y][r] += acc[x][y][r]; acc[x][y][r] = 0.f; }
   }
 
-  // ---- epilogue: drop padded groups, G x G max pool, causal store ----
+  // ---- split: store this part's raw group sums (pool_kernel finishes) ----
   // D[row = query group][col = key group]; lane: col l32, rows 8(r/4)+4hi+r%4
+  if (a.split > 1) {
+    float* dst = a.partials + (int64_t)blockIdx.x * (BM * BN);
+#pragma unroll
+    for (int x = 0; x < XB; ++x)
+#pragma unroll
+      for (int y = 0; y < 4; ++y)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = (BM / NW) * wave + 32 * x + 8 * (r >> 2) + 4 * hi + (r & 3);
+          dst[row * BN + 32 * y + l32] = tot[x][y][r];
+        }
+    return;
+  }
+
+  // ---- epilogue: drop padded groups, G x G max pool, causal store ----
   float* srow_base = a.scores + R.score_off + (int64_t)p * R.l_q * R.l_kv;
 #pragma unroll
   for (int x = 0; x < XB; ++x) {
@@ -346,6 +374,85 @@ __global__ void __launch_bounds__(NT, 1) scores_kernel(ScoreArgs a) {
         if (j * a.b <= e_i) srow_base[(int64_t)i * R.l_kv + j] = pr[r];
       }
     }
+  }
+}
+
+// Finish of a split score tile, POOL_ROWS group rows per workgroup: the
+// group sums of the `split` parts are added in part order (into LDS), then
+// padded groups are dropped, each G x G group block is max-pooled into its
+// block score (eq10) and the causal blocks are stored (eq11-eq14) -- what
+// the epilogue of an unsplit tile does.
+constexpr int POOL_ROWS = 32;
+constexpr int POOL_THREADS = 256;
+
+template <int G>
+__global__ void __launch_bounds__(POOL_THREADS) pool_kernel(ScoreArgs a) {
+  __shared__ float sum[POOL_ROWS][BN + 4];
+  constexpr int CHUNKS = BM / POOL_ROWS;
+  const int tile_id = blockIdx.x / CHUNKS;
+  const int chunk = blockIdx.x % CHUNKS;
+  const int ri = find_req(a.batch, tile_id);
+  const ReqDesc& R = a.batch.r[ri];
+  const int n_q = R.n_q, n_kv = R.n_kv;
+  const int local = tile_id - R.work_begin;
+  const int nqg = (n_q + a.g - 1) / a.g;
+  const int nkg = (n_kv + a.g - 1) / a.g;
+  const int ntj = col_tiles(nkg);
+  const int h = local % a.h_kv;
+  const int pm = (local / a.h_kv) % a.m;
+  const int rank = local / a.h_q;
+  const int ti = rank / ntj, tj = rank % ntj;
+  const int p = h * a.m + pm;
+  const int n_c = n_kv - n_q;
+  {
+    int gi_last = min(nqg, (ti + 1) * BM) - 1;
+    int i_max = gi_last / G;
+    int e_i = min(n_c + (i_max + 1) * a.b - 1, n_kv - 1);
+    int j_min = (tj * BN) / G;
+    if (j_min * a.b > e_i) return;   // no causal block pair: no part ran
+  }
+  const int row0 = chunk * POOL_ROWS;             // first group row of this chunk
+  if (ti * BM + row0 >= nqg) return;              // only padding rows
+  const int64_t part_stride = (int64_t)a.total_tiles * (BM * BN);
+  const float* src = a.partials + (int64_t)tile_id * (BM * BN) + (int64_t)row0 * BN;
+  // 1. the parts' group sums, in part order, 4 columns per thread
+  for (int e = threadIdx.x; e < POOL_ROWS * (BN / 4); e += POOL_THREADS) {
+    const int r = e / (BN / 4), c4 = e % (BN / 4);
+    const float* s0 = src + r * BN + 4 * c4;
+    float4 v = *reinterpret_cast<const float4*>(s0);
+    for (int q = 1; q < a.split; ++q) {
+      const float4 w = *reinterpret_cast<const float4*>(s0 + q * part_stride);
+      v.x += w.x;
+      v.y += w.y;
+      v.z += w.z;
+      v.w += w.w;
+    }
+    sum[r][4 * c4] = v.x;
+    sum[r][4 * c4 + 1] = v.y;
+    sum[r][4 * c4 + 2] = v.z;
+    sum[r][4 * c4 + 3] = v.w;
+  }
+  __syncthreads();
+  // 2. G x G max pool of real groups, causal store
+  float* srow_base = a.scores + R.score_off + (int64_t)p * R.l_q * R.l_kv;
+  constexpr int PI = POOL_ROWS / G, PJ = BN / G;
+  for (int o = threadIdx.x; o < PI * PJ; o += POOL_THREADS) {
+    const int ii = o / PJ, jj = o % PJ;
+    const int i = (ti * BM + row0) / G + ii, j = tj * PJ + jj;
+    if (i >= R.l_q || j >= R.l_kv) continue;
+    const int e_i = min(n_c + (i + 1) * a.b - 1, n_kv - 1);
+    if (j * a.b > e_i) continue;
+    float best = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int gi = ti * BM + row0 + ii * G + u;
+#pragma unroll
+      for (int v = 0; v < G; ++v) {
+        const int gj = tj * BN + jj * G + v;
+        if (gi < nqg && gj < nkg) best = fmaxf(best, sum[ii * G + u][jj * G + v]);
+      }
+    }
+    srow_base[(int64_t)i * R.l_kv + j] = best;
   }
 }
 
@@ -452,10 +559,15 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
 
 template <int G>
 hipError_t launch_scores(const ScoreArgs& a, int n_tiles, hipStream_t s) {
+  const dim3 grid((unsigned)((int64_t)n_tiles * a.split));
   if (a.kv.paged)
-    hipLaunchKernelGGL((scores_kernel<G, true>), dim3(n_tiles), dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((scores_kernel<G, true>), grid, dim3(NT), 0, s, a);
   else
-    hipLaunchKernelGGL((scores_kernel<G, false>), dim3(n_tiles), dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((scores_kernel<G, false>), grid, dim3(NT), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.split == 1) return e;
+  hipLaunchKernelGGL((pool_kernel<G>), dim3((unsigned)n_tiles * (BM / POOL_ROWS)),
+                     dim3(POOL_THREADS), 0, s, a);
   return hipGetLastError();
 }
 
@@ -470,6 +582,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
   a.q_st = L.q_st;
   a.kv = L.kv;
   a.scores = L.scores;
+  a.partials = L.partials;
   a.h_q = L.h_q;
   a.h_kv = L.h_kv;
   a.m = m;
@@ -487,6 +600,12 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
     const int nqg = (d.n_q + a.g - 1) / a.g, nkg = (d.n_kv + a.g - 1) / a.g;
     n_tiles += a.h_q * row_tiles(nqg) * col_tiles(nkg);
   }
+  const int n_stage = a.gc / BK;
+  a.split = L.split;
+  a.total_tiles = n_tiles;
+  if (a.split < 1 || (a.split > 1 && (n_stage % (a.split * CHAIN) != 0 || !a.partials)))
+    return hipErrorInvalidValue;
+  a.part_stages = n_stage / a.split;
   hipError_t e;
   switch (a.G) {
     case 1: e = launch_scores<1>(a, n_tiles, stream); break;

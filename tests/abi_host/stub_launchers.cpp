@@ -79,6 +79,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t) {
   ++g_launches[2];
   check_batch(L.batch, L.block);
   if (!L.block_mask || !L.scores || !L.q || !L.kv.k) ++g_bad;
+  if (L.split < 1 || (L.split > 1 && !L.partials)) ++g_bad;
   if (!estimate_supported(L.head_dim, L.block, L.group) || L.h_q / L.h_kv > 8) ++g_bad;
   int64_t mask = 0, score = 0;
   for (int r = 0; r < L.batch.n_req; ++r) {

@@ -47,6 +47,7 @@ class GuardedBuffers:
         cap = bfla.bfla_list_capacity(prob, prm)
         self.cap = cap
         ws = bfla.bfla_workspace_size(prob, prm, bfla.BFLA_WS_EXPAND)
+        ws_est = bfla.bfla_workspace_size(prob, prm, bfla.BFLA_WS_ESTIMATE)
         n_lse = sum(prob.c.h_q * n for n in prob.n_q)
         self.g = {
             "block_mask": Guarded(max(cap.mask_bytes, 1), torch.uint8, fill=9),
@@ -54,6 +55,7 @@ class GuardedBuffers:
             "row_ptr": Guarded(cap.n_rows + 1, torch.int32, fill=-5),
             "cols": Guarded(max(cap.max_cols, 1), torch.int32, fill=-7),
             "ws_expand": Guarded(max(ws, 16), torch.uint8),
+            "ws_estimate": Guarded(max(ws_est, 16), torch.uint8),
             "lse": Guarded(n_lse, torch.float32, fill=float("nan")),
         }
         if head_mask:

@@ -68,7 +68,7 @@ def test_capacity_and_workspace_sizes():
     assert cap.max_cols == 2 * (4 * 5 // 2) + 2 * (5 * 6 // 2)
     assert cap.mask_bytes == 2 * 2 * 2 + 2 * 3 * 3
     assert cap.score_elems == 4 * 2 * 2 + 4 * 3 * 3
-    assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE) == cap.score_elems * 4
+    assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE) >= cap.score_elems * 4
     assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) >= cap.n_rows * 4
     chunk = bfla.Problem([64], [320], 4, 2, 64)
     cap2 = bfla.bfla_list_capacity(chunk, prm)
@@ -252,3 +252,56 @@ def test_noalloc_tile_stage_rejects_problems_beyond_its_scratch():
     for n in ([131072], [16384, 32768, 65536, 131072]):
         p = bfla.Problem(n, n, 40, 8, 128)
         assert bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_EXPAND) <= bfla.EXPAND_SCRATCH_BYTES
+
+
+def _split_of(n, h_q, h_kv, c, **kw):
+    """The split of the Stage-1 score GEMM, read off the workspace size:
+    align256(split x tiles x 256 x 128 x 4 B) of partial sums + the scores."""
+    p = bfla.Problem(n, n, h_q, h_kv, c)
+    prm = bfla.params(**kw)
+    ws = bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE)
+    part = ws - bfla.bfla_list_capacity(p, prm).score_elems * 4
+    g = kw.get("group", 64)
+    tiles = sum(h_q * -(-(-(-x // g)) // 256) * -(-(-(-x // g)) // 128) for x in n)
+    if part == 0:
+        return 1
+    split = part // (tiles * 256 * 128 * 4)
+    assert part == split * tiles * 256 * 128 * 4, (part, tiles)
+    return split
+
+
+def test_stage1_split_follows_the_tile_count():
+    # 128K x 32 heads: 2304 causal score tiles, nine full rounds of 256
+    # workgroups -> no split, the workspace is just the scores
+    assert _split_of([131072], 32, 8, 128) == 1
+    # 32K x 32 heads: 192 causal tiles; four parts would run three rounds of
+    # quarter length, but their partial sums eat the gain -> no split
+    assert _split_of([32768], 32, 8, 128) == 1
+    # 64K x 16 heads at head dim 256: 320 causal tiles -> four parts (five rounds)
+    assert _split_of([65536], 16, 8, 256) == 4
+    # a 2K request: 4 tiles -> eight parts, the most whole 8-stage chains allow
+    assert _split_of([2048], 4, 2, 64) == 8
+    # 16 stages (g C = 1024) hold two chains: at most two parts
+    assert _split_of([2048], 4, 2, 64, block=128, group=16) == 2
+    # the paged batch (4 requests, 40 heads) fills the GPU unsplit
+    assert _split_of([16384, 32768, 65536, 131072], 40, 8, 128) == 1
+
+
+def test_estimate_workspace_is_checked():
+    L = bfla.lib()
+    p, prm = _prob(), bfla.params()   # small: split, so partial sums are needed
+    v, kv = _fake_views()
+    addr = C.c_void_p(1 << 20)
+    ws = bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE)
+    scores = bfla.bfla_list_capacity(p, prm).score_elems * 4
+    # with dbg_scores the partial sums still need the workspace
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, addr,
+                              None, None, 0, None)
+    assert st == bfla.BFLA_ERR_WORKSPACE
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, addr,
+                              None, addr, ws - scores - 1, None)
+    assert st == bfla.BFLA_ERR_WORKSPACE
+    # misaligned workspace
+    st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, addr,
+                              None, C.c_void_p((1 << 20) + 16), ws, None)
+    assert st == bfla.BFLA_ERR_INVALID_ARG

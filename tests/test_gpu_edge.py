@@ -23,7 +23,7 @@ def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
     prm = bfla.params(**KW)
     buf = GuardedBuffers(db.prob, prm, head_mask=True)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
-                            dbg_head_mask=buf.head_mask)
+                            dbg_head_mask=buf.head_mask, workspace=buf.ws_estimate)
     torch.cuda.synchronize()
     buf.check("estimate_mask")
     bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)

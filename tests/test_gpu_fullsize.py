@@ -53,7 +53,8 @@ class Contig:
         buf = bfla.Buffers(self.prob, prm)
         head = torch.empty(max(buf.cap.score_elems, 1), dtype=torch.uint8, device="cuda")
         bfla.bfla_estimate_mask(self.prob, prm, self.qv, self.kv, buf.block_mask,
-                                dbg_scores=buf.scores, dbg_head_mask=head)
+                                dbg_scores=buf.scores, dbg_head_mask=head,
+                                workspace=buf.ws_estimate)
         bfla.bfla_expand_rescue(self.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
                                 buf.ws_expand)
         torch.cuda.synchronize()
@@ -233,7 +234,7 @@ def test_paged_4x_per_request():
     buf = bfla.Buffers(pb.prob, prm)
     head = torch.empty(buf.cap.score_elems, dtype=torch.uint8, device="cuda")
     bfla.bfla_estimate_mask(pb.prob, prm, pb.qv, pb.kv, buf.block_mask, dbg_scores=buf.scores,
-                            dbg_head_mask=head)
+                            dbg_head_mask=head, workspace=buf.ws_estimate)
     bfla.bfla_expand_rescue(pb.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
     torch.cuda.synchronize()
     rp = buf.row_ptr.cpu().numpy()

@@ -34,7 +34,8 @@ def test_paged_equals_contiguous_and_oracle(shape):
     outs = []
     for b in (pb, db):
         buf = bfla.Buffers(b.prob, prm)
-        bfla.bfla_estimate_mask(b.prob, prm, b.qv, b.kv, buf.block_mask, dbg_scores=buf.scores)
+        bfla.bfla_estimate_mask(b.prob, prm, b.qv, b.kv, buf.block_mask, dbg_scores=buf.scores,
+                                workspace=buf.ws_estimate)
         bfla.bfla_expand_rescue(b.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
                                 buf.ws_expand)
         torch.cuda.synchronize()

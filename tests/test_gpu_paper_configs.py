@@ -42,7 +42,8 @@ def test_paper_config_end_to_end(cfg):
               rho=rho, seed=wl.seed)
     prm = bfla.params(**kw)
     buf = bfla.Buffers(db.prob, prm)
-    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
+                            workspace=buf.ws_estimate)
     bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
     torch.cuda.synchronize()
     rp_gpu = buf.row_ptr.cpu().numpy()

@@ -157,7 +157,7 @@ def test_estimate_mask_matches_oracle(shape, gamma):
     st = _oracle_stage1(db, kw)
     buf = GuardedBuffers(db.prob, prm, head_mask=True)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
-                            dbg_head_mask=buf.head_mask)
+                            dbg_head_mask=buf.head_mask, workspace=buf.ws_estimate)
     torch.cuda.synchronize()
     buf.check("estimate_mask")
     got_mask = buf.block_mask.cpu().numpy()
@@ -186,21 +186,24 @@ def test_estimate_mask_matches_oracle(shape, gamma):
 def test_head_mask_is_optional_and_changes_nothing():
     """The per-head output is a debug view: the block mask and scores are the
     same bit for bit with and without it, and without dbg_scores the scores
-    go to the workspace."""
+    go to the workspace, after the split score GEMM's partial sums."""
     db = _make(*SHAPES[5])
     kw, prm = _params()
     a = GuardedBuffers(db.prob, prm, head_mask=True)
     b = GuardedBuffers(db.prob, prm)
-    ws = Guarded(bfla.bfla_workspace_size(db.prob, prm, bfla.BFLA_WS_ESTIMATE), torch.uint8)
+    n_ws = bfla.bfla_workspace_size(db.prob, prm, bfla.BFLA_WS_ESTIMATE)
+    ws = Guarded(n_ws, torch.uint8)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, a.block_mask, dbg_scores=a.scores,
-                            dbg_head_mask=a.head_mask)
+                            dbg_head_mask=a.head_mask, workspace=a.ws_estimate)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, b.block_mask, workspace=ws.t)
     torch.cuda.synchronize()
     a.check("with head mask")
     b.check("without")
     ws.check("estimate workspace")
     assert torch.equal(a.block_mask, b.block_mask)
-    assert torch.equal(a.scores.view(torch.int32), ws.t.view(torch.float32).view(torch.int32))
+    n_s = a.cap.score_elems
+    in_ws = ws.t[n_ws - 4 * n_s:].view(torch.int32)
+    assert torch.equal(a.scores.view(torch.int32), in_ws)
 
 
 @pytest.mark.parametrize("shape", [SHAPES[0], SHAPES[2], SHAPES[4], SHAPES[8]],
@@ -209,7 +212,8 @@ def test_end_to_end_pipeline(shape):
     db = _make(*shape)
     kw, prm = _params()
     buf = GuardedBuffers(db.prob, prm)
-    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+    bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
+                            workspace=buf.ws_estimate)
     torch.cuda.synchronize()
     buf.check("estimate_mask")
     bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
@@ -258,7 +262,8 @@ def test_runs_are_bit_identical():
     for _ in range(2):
         buf = bfla.Buffers(db.prob, prm)
         db.o.fill_(0)
-        bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores)
+        bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
+                                workspace=buf.ws_estimate)
         bfla.bfla_expand_rescue(db.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
                                 buf.ws_expand)
         torch.cuda.synchronize()

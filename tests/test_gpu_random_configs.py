@@ -73,7 +73,7 @@ def test_random_configuration_matches_oracle(case):
     prm = bfla.params(**kw)
     buf = GuardedBuffers(bt.prob, prm, head_mask=True)
     bfla.bfla_estimate_mask(bt.prob, prm, bt.qv, bt.kv, buf.block_mask, dbg_scores=buf.scores,
-                            dbg_head_mask=buf.head_mask)
+                            dbg_head_mask=buf.head_mask, workspace=buf.ws_estimate)
     torch.cuda.synchronize()
     buf.check("estimate_mask")
     bfla.bfla_expand_rescue(bt.prob, prm, buf.block_mask, buf.row_ptr, buf.cols, buf.ws_expand)
