@@ -172,6 +172,19 @@ def test_keep_mass_limits():
     assert np.all(keep0.sum(axis=1) == 1)
 
 
+def test_gamma_one_keeps_every_block_even_when_the_float_mass_saturates():
+    # one block carries all but ~1e-43 of the mass: its float32 mass rounds to
+    # 1.0, so a float running sum reaches gamma = 1 after one block; in exact
+    # arithmetic only the full set reaches 1, so all four are kept
+    s = np.array([[100.0, 0.0, 0.0, 0.0, -np.inf]], np.float32)
+    assert O.block_probs(s, 1.0)[0, 0] == np.float32(1.0)
+    keep, _, r = O.keep_mass(s, 1.0, 1.0)
+    assert r[0] == 4 and keep[0].tolist() == [True, True, True, True, False]
+    # just below 1 the saturated float mass already reaches gamma
+    keep, _, r = O.keep_mass(s, 0.999999, 1.0)
+    assert r[0] == 1
+
+
 def test_keep_mass_tie_break_by_index():
     s = np.array([[5.0, 7.0, 7.0, 7.0, -np.inf]], np.float32)
     keep, tie, r = O.keep_mass(s, 0.5, 1.0)

@@ -126,6 +126,19 @@ def test_rho_threshold_integer_compare():
     assert abs(float((v < O.rho_threshold(0.25)).mean()) - 0.25) < 0.005
 
 
+def test_random_rescue_threshold_is_strict():
+    # eq25 rescues a dropped tile iff psi < rho: with rho set to exactly the
+    # tile's psi the tile stays dropped, one step of 2^-24 above it is rescued
+    n, h, seed = 3 * 64, 1, 77
+    bm = np.zeros((2, 2), np.uint8)
+    v = int(O.psi24(h, 2, 0, seed))
+    args = dict(n_local=-1, n_sink=0, eta=0, seed=seed, h=h)
+    at = O.tile_mask(bm, n, n, 128, 64, rho=v / 16777216.0, **args)
+    above = O.tile_mask(bm, n, n, 128, 64, rho=(v + 1) / 16777216.0, **args)
+    assert O.rho_threshold(v / 16777216.0) == v
+    assert not at[2, 0] and above[2, 0]
+
+
 def test_lists_are_ascending_rows_in_order():
     n = [300, 1000]
     masks = [np.tril(np.ones((3, 3), np.uint8))[None].repeat(2, 0) * 0,
