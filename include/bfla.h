@@ -51,9 +51,10 @@ extern "C" {
 #endif
 
 #define BFLA_VERSION_STRING "0.2.0"
-/* Maximum number of requests per call (descriptors travel in kernel
- * arguments). */
-#define BFLA_MAX_BATCH 32
+/* Maximum number of requests per call.  The kernels take the descriptors of
+ * up to 32 requests in their arguments, so a larger batch launches each
+ * kernel once per group of 32 requests. */
+#define BFLA_MAX_BATCH 65536
 
 typedef enum bfla_status {
   BFLA_OK = 0,

@@ -11,7 +11,7 @@ BFLA_OK, BFLA_ERR_INVALID_ARG, BFLA_ERR_UNSUPPORTED = 0, 1, 2
 BFLA_ERR_WORKSPACE, BFLA_ERR_CAPACITY, BFLA_ERR_HIP = 3, 4, 5
 BFLA_KV_CONTIGUOUS, BFLA_KV_PAGED = 0, 1
 BFLA_WS_ESTIMATE, BFLA_WS_EXPAND = 1, 2
-MAX_BATCH = 32
+MAX_BATCH = 65536
 EXPAND_SCRATCH_BYTES = 16 << 20
 
 

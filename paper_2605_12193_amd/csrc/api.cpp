@@ -206,13 +206,13 @@ int64_t view_off(const bfla_view* v, int r) {
 }
 
 // Request descriptors in request order (offsets of every packed output).
-Batch make_batch(const bfla_problem* prob, const bfla_params* pr, const bfla_view* q,
-                 const bfla_view* o, const bfla_kv* kv) {
-  Batch b{};
-  b.n_req = prob->batch;
+std::vector<ReqDesc> make_batch(const bfla_problem* prob, const bfla_params* pr,
+                                const bfla_view* q, const bfla_view* o, const bfla_kv* kv) {
+  std::vector<ReqDesc> b((size_t)prob->batch);
   int64_t row = 0, mask = 0, score = 0, lse = 0;
   for (int r = 0; r < prob->batch; ++r) {
-    ReqDesc& d = b.r[r];
+    ReqDesc& d = b[(size_t)r];
+    d = ReqDesc{};
     d.n_q = prob->n_q[r];
     d.n_kv = prob->n_kv[r];
     d.l_q = (int32_t)cdiv(d.n_q, pr->block);
@@ -238,11 +238,30 @@ Batch make_batch(const bfla_problem* prob, const bfla_params* pr, const bfla_vie
 }
 
 // Longest requests first (their rows are the longest work items).
-Batch longest_first(const Batch& in) {
-  Batch b = in;
-  std::stable_sort(b.r, b.r + b.n_req,
+std::vector<ReqDesc> longest_first(std::vector<ReqDesc> b) {
+  std::stable_sort(b.begin(), b.end(),
                    [](const ReqDesc& x, const ReqDesc& y) { return x.n_kv > y.n_kv; });
   return b;
+}
+
+// Stage 1 runs once per group of kLaunchRequests requests (in request order),
+// each group with its own split of the score GEMM; the groups share one
+// partial-sum buffer in stream order, sized for the largest.
+struct Stage1Layout {
+  std::vector<int32_t> splits;
+  size_t partial_bytes = 0;
+};
+
+Stage1Layout stage1_layout(const bfla_problem* prob, const bfla_params* pr) {
+  Stage1Layout lay;
+  for (int g0 = 0; g0 < prob->batch; g0 += kLaunchRequests) {
+    const int n = std::min(kLaunchRequests, prob->batch - g0);
+    const EstimatePlan plan = estimate_plan(prob->n_q + g0, prob->n_kv + g0, n, prob->h_q,
+                                            prob->head_dim, pr->block, pr->group);
+    lay.splits.push_back(plan.split);
+    lay.partial_bytes = std::max(lay.partial_bytes, plan.partial_bytes);
+  }
+  return lay;
 }
 
 float scale_of(const bfla_problem* prob, const bfla_params* pr) {
@@ -282,13 +301,13 @@ int prefill_common(const bfla_problem* prob, const bfla_params* pr, const bfla_v
   L->h_kv = prob->h_kv;
   L->head_dim = prob->head_dim;
   L->scale = scale_of(prob, pr);
-  L->batch = longest_first(make_batch(prob, pr, q, o, kv));
+  L->reqs = longest_first(make_batch(prob, pr, q, o, kv));
   return BFLA_OK;
 }
 
 // Stage-1 workspace: the partial sums of a split score GEMM first, then the
 // block scores when the caller passes no dbg_scores.
-size_t estimate_ws_scores_offset(const EstimatePlan& plan) {
+size_t estimate_ws_scores_offset(const Stage1Layout& plan) {
   return (plan.partial_bytes + 255) / 256 * 256;
 }
 
@@ -335,7 +354,7 @@ int expand_common(const bfla_problem* prob, const bfla_params* params,
   L.eta = params->eta;
   L.rho24 = (uint32_t)floor(params->rho * 16777216.0);
   L.seed = params->seed;
-  L.batch = make_batch(prob, params, nullptr, nullptr, nullptr);
+  L.reqs = make_batch(prob, params, nullptr, nullptr, nullptr);
   return hip_status(launch_expand(L, static_cast<hipStream_t>(stream)),
                     use_scratch ? "expand_rescue_noalloc" : "expand_rescue");
 }
@@ -382,9 +401,8 @@ int bfla_workspace_size(const bfla_problem* prob, const bfla_params* params, int
     if (!estimate_supported(prob->head_dim, params->block, params->group))
       return fail(BFLA_ERR_UNSUPPORTED, "block %d / group %d not built for head_dim %d",
                   params->block, params->group, prob->head_dim);
-    const EstimatePlan plan = estimate_plan(prob->n_q, prob->n_kv, prob->batch, prob->h_q,
-                                            prob->head_dim, params->block, params->group);
-    *bytes = estimate_ws_scores_offset(plan) + (size_t)s.score_elems * sizeof(float);
+    *bytes = estimate_ws_scores_offset(stage1_layout(prob, params)) +
+             (size_t)s.score_elems * sizeof(float);
   } else if (which == BFLA_WS_EXPAND) {
     *bytes = expand_workspace_bytes(s.n_rows, s.max_t_kv);
   } else {
@@ -419,8 +437,7 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
       return fail(BFLA_ERR_UNSUPPORTED, "request %d: more than %d KV blocks", r,
                   (int)kMaxBlocksPerRow);
   Sizes s = sizes_of(prob, params);
-  const EstimatePlan plan = estimate_plan(prob->n_q, prob->n_kv, prob->batch, prob->h_q,
-                                          prob->head_dim, params->block, params->group);
+  Stage1Layout plan = stage1_layout(prob, params);
   const size_t off = estimate_ws_scores_offset(plan);
   const size_t need = dbg_scores ? plan.partial_bytes : off + (size_t)s.score_elems * sizeof(float);
   if (need > 0 && (!workspace || ws_bytes < need))
@@ -436,8 +453,8 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   L.kv = kv_addr(kv);
   L.block_mask = block_mask;
   L.scores = scores;
-  L.partials = plan.split > 1 ? static_cast<float*>(workspace) : nullptr;
-  L.split = plan.split;
+  L.partials = plan.partial_bytes > 0 ? static_cast<float*>(workspace) : nullptr;
+  L.splits = std::move(plan.splits);
   L.head_mask = dbg_head_mask;
   L.h_q = prob->h_q;
   L.h_kv = prob->h_kv;
@@ -446,7 +463,7 @@ int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params, cons
   L.group = params->group;
   L.gamma = params->gamma;
   L.alpha = scale_of(prob, params);
-  L.batch = make_batch(prob, params, q, nullptr, kv);
+  L.reqs = make_batch(prob, params, q, nullptr, kv);
   return hip_status(launch_estimate(L, static_cast<hipStream_t>(stream)), "estimate_mask");
 }
 

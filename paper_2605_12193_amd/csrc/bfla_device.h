@@ -32,10 +32,15 @@ struct ReqDesc {
   int32_t pad_;
 };
 
+// Requests per kernel launch: their descriptors travel in the kernel
+// arguments, so a call with more requests launches each kernel once per
+// group of this many (in the launch order of its entry point).
+constexpr int kLaunchRequests = 32;
+
 struct Batch {
   int32_t n_req;
   int32_t pad_[3];
-  ReqDesc r[BFLA_MAX_BATCH];
+  ReqDesc r[kLaunchRequests];
 };
 
 // K/V addressing shared by every kernel that reads keys or values.
@@ -52,11 +57,14 @@ struct KvAddr {
   int32_t pad_;
 };
 
-// Request owning work item `w` (requests are laid out by work_begin).
+// Request owning work item `w`: the last request whose first item is at or
+// before w (work_begin ascends over the requests of a launch); a binary
+// search over at most kLaunchRequests descriptors.
 __device__ __forceinline__ int find_req(const Batch& b, int w) {
   int r = 0;
-  for (int i = 1; i < b.n_req; ++i)
-    if (w >= b.r[i].work_begin) r = i;
+#pragma unroll
+  for (int step = kLaunchRequests / 2; step >= 1; step >>= 1)
+    if (r + step < b.n_req && w >= b.r[r + step].work_begin) r += step;
   return r;
 }
 

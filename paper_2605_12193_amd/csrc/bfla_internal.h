@@ -5,6 +5,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <vector>
+
 #include "bfla_device.h"
 
 namespace bfla {
@@ -45,7 +47,7 @@ struct PrefillLaunch {
   KvAddr kv;
   int32_t h_q, h_kv, head_dim;
   float scale;
-  Batch batch;  // requests in launch order (longest first)
+  std::vector<ReqDesc> reqs;  // every request, in launch order (longest first)
 };
 
 bool prefill_supported(int head_dim, int m);
@@ -65,7 +67,7 @@ struct ExpandLaunch {
   int32_t n_local, n_sink, eta;
   uint32_t rho24;    // floor(rho * 2^24); 1<<24 means every dropped tile
   uint64_t seed;
-  Batch batch;       // requests in request order
+  std::vector<ReqDesc> reqs;  // every request, in request order
 };
 
 hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream);
@@ -81,13 +83,13 @@ struct EstimateLaunch {
   uint8_t* block_mask;
   float* scores;      // [per request H_q x L_q x L_kv], workspace or dbg output
   float* partials;    // split > 1: [split][tiles][kScoreTileM][kScoreTileN] raw group sums
-  int32_t split;
   uint8_t* head_mask; // [per request H_q x L_q x L_kv] per-head keep sets, or null
   int32_t h_q, h_kv, head_dim;
   int32_t block, group;
   float gamma;
   float alpha;
-  Batch batch;        // requests in request order
+  std::vector<ReqDesc> reqs;    // every request, in request order
+  std::vector<int32_t> splits;  // split of each group of kLaunchRequests requests
 };
 
 bool estimate_supported(int head_dim, int block, int group);

@@ -25,6 +25,8 @@
 // (score descending, block index ascending) with a sequential float
 // running mass (eq16-eq18), then OR of the m heads into the u8 mask row.
 // On request each wave also stores its own head's keep set (eq18).
+#include <algorithm>
+
 #include "bfla_device.h"
 #include "bfla_internal.h"
 
@@ -591,31 +593,7 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
   a.b = L.block;
   a.G = L.block / L.group;
   a.gc = L.group * L.head_dim;
-  a.batch = L.batch;
-  int n_tiles = 0;
-  for (int r = 0; r < a.batch.n_req; ++r) {
-    ReqDesc& d = a.batch.r[r];
-    if (d.l_kv > MAX_LKV) return hipErrorInvalidValue;
-    d.work_begin = n_tiles;
-    const int nqg = (d.n_q + a.g - 1) / a.g, nkg = (d.n_kv + a.g - 1) / a.g;
-    n_tiles += a.h_q * row_tiles(nqg) * col_tiles(nkg);
-  }
   const int n_stage = a.gc / BK;
-  a.split = L.split;
-  a.total_tiles = n_tiles;
-  if (a.split < 1 || (a.split > 1 && (n_stage % (a.split * CHAIN) != 0 || !a.partials)))
-    return hipErrorInvalidValue;
-  a.part_stages = n_stage / a.split;
-  hipError_t e;
-  switch (a.G) {
-    case 1: e = launch_scores<1>(a, n_tiles, stream); break;
-    case 2: e = launch_scores<2>(a, n_tiles, stream); break;
-    case 4: e = launch_scores<4>(a, n_tiles, stream); break;
-    case 8: e = launch_scores<8>(a, n_tiles, stream); break;
-    case 16: e = launch_scores<16>(a, n_tiles, stream); break;
-    default: return hipErrorInvalidValue;
-  }
-  if (e != hipSuccess) return e;
 
   SelectArgs s;
   s.scores = L.scores;
@@ -628,14 +606,53 @@ hipError_t launch_estimate(const EstimateLaunch& L, hipStream_t stream) {
   s.b = L.block;
   s.gamma = L.gamma;
   s.alpha = L.alpha;
-  s.batch = L.batch;
-  int n_rows = 0;
-  for (int r = 0; r < s.batch.n_req; ++r) {
-    s.batch.r[r].work_begin = n_rows;
-    n_rows += L.h_kv * s.batch.r[r].l_q;
+
+  // scores (and their pooling when split) then the selection, once per group
+  // of kLaunchRequests requests; the groups share the partial-sum buffer in
+  // stream order
+  const size_t n_groups = (L.reqs.size() + kLaunchRequests - 1) / kLaunchRequests;
+  if (L.splits.size() != n_groups) return hipErrorInvalidValue;
+  for (size_t gi = 0; gi < n_groups; ++gi) {
+    const size_t g0 = gi * kLaunchRequests;
+    const int n = (int)std::min<size_t>(kLaunchRequests, L.reqs.size() - g0);
+    a.batch.n_req = n;
+    int n_tiles = 0;
+    for (int r = 0; r < n; ++r) {
+      ReqDesc& d = a.batch.r[r];
+      d = L.reqs[g0 + r];
+      if (d.l_kv > MAX_LKV) return hipErrorInvalidValue;
+      d.work_begin = n_tiles;
+      const int nqg = (d.n_q + a.g - 1) / a.g, nkg = (d.n_kv + a.g - 1) / a.g;
+      n_tiles += a.h_q * row_tiles(nqg) * col_tiles(nkg);
+    }
+    a.split = L.splits[gi];
+    a.total_tiles = n_tiles;
+    if (a.split < 1 || (a.split > 1 && (n_stage % (a.split * CHAIN) != 0 || !a.partials)))
+      return hipErrorInvalidValue;
+    a.part_stages = n_stage / a.split;
+    hipError_t e;
+    switch (a.G) {
+      case 1: e = launch_scores<1>(a, n_tiles, stream); break;
+      case 2: e = launch_scores<2>(a, n_tiles, stream); break;
+      case 4: e = launch_scores<4>(a, n_tiles, stream); break;
+      case 8: e = launch_scores<8>(a, n_tiles, stream); break;
+      case 16: e = launch_scores<16>(a, n_tiles, stream); break;
+      default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+
+    s.batch.n_req = n;
+    int n_rows = 0;
+    for (int r = 0; r < n; ++r) {
+      s.batch.r[r] = L.reqs[g0 + r];
+      s.batch.r[r].work_begin = n_rows;
+      n_rows += L.h_kv * s.batch.r[r].l_q;
+    }
+    hipLaunchKernelGGL(select_kernel, dim3(n_rows), dim3(64 * m), 0, stream, s);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(select_kernel, dim3(n_rows), dim3(64 * m), 0, stream, s);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace bfla

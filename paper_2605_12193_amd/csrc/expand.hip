@@ -11,6 +11,7 @@
 // the row counts; pass 2 is an exclusive scan of the counts in one
 // workgroup; pass 3 reads the ballots back and writes each kept tile at its
 // list position, so every keep / drop decision is taken once.
+#include <algorithm>
 #include <atomic>
 
 #include "bfla_device.h"
@@ -43,6 +44,7 @@ struct ExpandArgs {
   uint32_t rho24;
   uint64_t chi_key;  // mix64(s)
   uint64_t psi_key;  // mix64(s + 1)
+  int32_t row_lo, row_hi;  // list rows of this launch's requests
   Batch batch;
 };
 
@@ -59,10 +61,12 @@ struct RowCtx {
 };
 
 __device__ __forceinline__ bool row_ctx(const ExpandArgs& a, int row, RowCtx* c) {
-  if (row >= a.n_rows) return false;
+  if (row >= a.row_hi) return false;
+  // the request owning the row: row_base ascends over the launch's requests
   int ri = 0;
-  for (int i = 1; i < a.batch.n_req; ++i)
-    if (row >= a.batch.r[i].row_base) ri = i;
+#pragma unroll
+  for (int step = kLaunchRequests / 2; step >= 1; step >>= 1)
+    if (ri + step < a.batch.n_req && row >= a.batch.r[ri + step].row_base) ri += step;
   const ReqDesc& R = a.batch.r[ri];
   int local = row - R.row_base;
   c->h = local / R.t_q;
@@ -98,7 +102,7 @@ __device__ __forceinline__ bool keep_tile(const ExpandArgs& a, const RowCtx& c, 
 
 __global__ void __launch_bounds__(64 * ROWS_PER_WG) count_kernel(ExpandArgs a) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
+  const int row = a.row_lo + blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
   RowCtx c;
   if (!row_ctx(a, row, &c)) return;
   uint64_t* bits = a.bits + (int64_t)row * a.words_per_row;
@@ -146,7 +150,7 @@ __global__ void __launch_bounds__(SCAN_THREADS) scan_kernel(const int32_t* count
 
 __global__ void __launch_bounds__(64 * ROWS_PER_WG) scatter_kernel(ExpandArgs a) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
+  const int row = a.row_lo + blockIdx.x * ROWS_PER_WG + (threadIdx.x >> 6);
   RowCtx c;
   if (!row_ctx(a, row, &c)) return;
   const uint64_t* bits = a.bits + (int64_t)row * a.words_per_row;
@@ -207,17 +211,35 @@ hipError_t launch_expand(const ExpandLaunch& L, hipStream_t stream) {
   a.rho24 = L.rho24;
   a.chi_key = mix64(L.seed);
   a.psi_key = mix64(L.seed + 1);
-  a.batch = L.batch;
-  const int grid = (L.n_rows + ROWS_PER_WG - 1) / ROWS_PER_WG;
-  hipLaunchKernelGGL(count_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
-  hipError_t e = hipGetLastError();
+  // count and scatter once per group of kLaunchRequests requests (each over
+  // its own rows), one scan over every row in between
+  auto for_each_group = [&](auto&& launch) -> hipError_t {
+    for (size_t g0 = 0; g0 < L.reqs.size(); g0 += kLaunchRequests) {
+      const int n = (int)std::min<size_t>(kLaunchRequests, L.reqs.size() - g0);
+      a.batch.n_req = n;
+      for (int i = 0; i < n; ++i) a.batch.r[i] = L.reqs[g0 + i];
+      const ReqDesc& last = a.batch.r[n - 1];
+      a.row_lo = a.batch.r[0].row_base;
+      a.row_hi = last.row_base + L.h_kv * last.t_q;
+      if (a.row_hi == a.row_lo) continue;
+      const int grid = (a.row_hi - a.row_lo + ROWS_PER_WG - 1) / ROWS_PER_WG;
+      launch(grid);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  };
+  hipError_t e = for_each_group([&](int grid) {
+    hipLaunchKernelGGL(count_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
+  });
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, stream, a.counts, a.row_ptr,
                      a.n_rows);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
-  return hipGetLastError();
+  return for_each_group([&](int grid) {
+    hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(64 * ROWS_PER_WG), 0, stream, a);
+  });
 }
 
 }  // namespace bfla

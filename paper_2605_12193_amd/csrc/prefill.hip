@@ -40,6 +40,7 @@
 // taken, the running max moves up to it where it is larger (O and l
 // rescaled) and the weights are recomputed (all <= 1).  O and l always refer
 // to the same max, so O / l is exact.
+#include <algorithm>
 #include <atomic>
 #include <utility>
 
@@ -1325,22 +1326,30 @@ hipError_t launch_prefill(const PrefillLaunch& L, hipStream_t stream) {
   a.h_kv = L.h_kv;
   a.m = L.h_q / L.h_kv;
   a.scale = L.scale;
-  a.batch = L.batch;
   // work items per (request, KV head, q-tile): two for the half-tile shapes
   const int per_row = parts_per_row(L.head_dim, a.m);
-  int n_work = 0;
-  for (int i = 0; i < a.batch.n_req; ++i) {
-    a.batch.r[i].work_begin = n_work;
-    n_work += per_row * a.h_kv * a.batch.r[i].t_q;
-  }
-  if (n_work == 0) return hipSuccess;
   const bool dense = L.row_ptr == nullptr;
-  switch (L.head_dim) {
-    case 64: return launch_c<64>(a, dense, n_work, stream);
-    case 128: return launch_c<128>(a, dense, n_work, stream);
-    case 256: return launch_c<256>(a, dense, n_work, stream);
-    default: return hipErrorInvalidValue;
+  // one launch per group of kLaunchRequests requests (longest first)
+  for (size_t g0 = 0; g0 < L.reqs.size(); g0 += kLaunchRequests) {
+    const int n = (int)std::min<size_t>(kLaunchRequests, L.reqs.size() - g0);
+    a.batch.n_req = n;
+    int n_work = 0;
+    for (int i = 0; i < n; ++i) {
+      a.batch.r[i] = L.reqs[g0 + i];
+      a.batch.r[i].work_begin = n_work;
+      n_work += per_row * a.h_kv * a.batch.r[i].t_q;
+    }
+    if (n_work == 0) continue;
+    hipError_t e;
+    switch (L.head_dim) {
+      case 64: e = launch_c<64>(a, dense, n_work, stream); break;
+      case 128: e = launch_c<128>(a, dense, n_work, stream); break;
+      case 256: e = launch_c<256>(a, dense, n_work, stream); break;
+      default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
   }
+  return hipSuccess;
 }
 
 }  // namespace bfla

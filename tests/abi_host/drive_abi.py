@@ -93,7 +93,7 @@ def random_case(rng, L):
         """A valid choice, or now and then an invalid one."""
         return rng.choice(invalid) if invalid and rng.random() < p_bad else rng.choice(valid)
 
-    batch = pick([1, 1, 2, 3, 7, 32], [0, 33])
+    batch = pick([1, 1, 2, 3, 7, 32, 33, 70], [0, 65537])
     c = pick([64, 128, 256], [96])
     h_kv = rng.choice([1, 2, 8])
     m = pick([1, 2, 4, 5, 8], [9])

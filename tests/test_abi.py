@@ -79,7 +79,7 @@ def test_capacity_and_workspace_sizes():
     (lambda p, q: setattr(p.c, "h_q", 5), bfla.BFLA_ERR_INVALID_ARG),
     (lambda p, q: setattr(p.c, "head_dim", 96), bfla.BFLA_ERR_UNSUPPORTED),
     (lambda p, q: setattr(p.c, "batch", 0), bfla.BFLA_ERR_INVALID_ARG),
-    (lambda p, q: setattr(p.c, "batch", 33), bfla.BFLA_ERR_INVALID_ARG),
+    (lambda p, q: setattr(p.c, "batch", 65537), bfla.BFLA_ERR_INVALID_ARG),
     (lambda p, q: setattr(q, "gamma", 0.0), bfla.BFLA_ERR_INVALID_ARG),
     (lambda p, q: setattr(q, "gamma", 1.5), bfla.BFLA_ERR_INVALID_ARG),
     (lambda p, q: setattr(q, "gamma", float("nan")), bfla.BFLA_ERR_INVALID_ARG),
@@ -305,3 +305,16 @@ def test_estimate_workspace_is_checked():
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(v), C.byref(kv), addr, addr,
                               None, C.c_void_p((1 << 20) + 16), ws, None)
     assert st == bfla.BFLA_ERR_INVALID_ARG
+
+
+def test_batches_beyond_one_launch_group_are_sized():
+    # 70 requests (three launch groups of up to 32): sizes are the sums over
+    # requests, and the Stage-1 workspace covers the largest group's split
+    prm = bfla.params()
+    n = [64 * (1 + i % 7) + i for i in range(70)]
+    p = bfla.Problem(n, n, 4, 2, 64)
+    cap = bfla.bfla_list_capacity(p, prm)
+    assert cap.n_rows == sum(2 * -(-x // 64) for x in n)
+    assert cap.mask_bytes == sum(2 * (-(-x // 128)) ** 2 for x in n)
+    ws = bfla.bfla_workspace_size(p, prm, bfla.BFLA_WS_ESTIMATE)
+    assert ws >= cap.score_elems * 4

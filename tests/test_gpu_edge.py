@@ -1,14 +1,16 @@
 """Degenerate and boundary inputs through the whole path against the oracle:
 sequences of 1, 2 and around one tile / one block, a single query against a
-long prefix, and the maximum batch of 32 requests of mixed lengths."""
+long prefix, a batch of 32 requests of mixed lengths (one launch group of
+request descriptors), and batches of 40 and 70 requests that every kernel
+runs as several launch groups (contiguous and paged K/V)."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
-from parity_util import (DeviceBatch, GuardedBuffers, compare_outputs, head_mask_compare,
-                         mask_compare, oracle_lists_for)
+from parity_util import (DeviceBatch, GuardedBuffers, PagedBatch, compare_outputs,
+                         head_mask_compare, mask_compare, oracle_lists_for)
 
 pytestmark = pytest.mark.gpu
 
@@ -16,10 +18,17 @@ KW = dict(block=128, group=64, tile=64, gamma=0.9, n_local=2, n_sink=1, eta=16, 
           seed=11)
 
 
-def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0):
+def _run(seqlens, n_q=None, h_q=4, h_kv=2, c=64, seed=0, page_size=None):
     wl = synth.workload("tiny_2k", h_q=h_q, h_kv=h_kv, head_dim=c, seed=seed)
     seqs = synth.make_inputs(wl, seqlens=seqlens)
-    db = DeviceBatch(seqs, n_q)
+    if page_size is None:
+        db = DeviceBatch(seqs, n_q)
+    else:
+        db = PagedBatch(seqs, n_q if n_q is not None else seqlens, page_size, seed)
+        s0 = seqs
+        db.h_q, db.h_kv, db.c = h_q, h_kv, c
+        db.host = lambda r: (s0[r].q[:, s0[r].q.shape[1] - db.n_q[r]:].double().numpy(),
+                             s0[r].k.double().numpy(), s0[r].v.double().numpy())
     prm = bfla.params(**KW)
     buf = GuardedBuffers(db.prob, prm, head_mask=True)
     bfla.bfla_estimate_mask(db.prob, prm, db.qv, db.kv, buf.block_mask, dbg_scores=buf.scores,
@@ -97,3 +106,19 @@ def test_max_batch_of_32_requests(c, h_q):
     seqlens = [int(x) for x in rng.integers(1, 700, size=32)]
     n_q = [max(1, int(n * f)) for n, f in zip(seqlens, rng.uniform(0.3, 1.0, size=32))]
     _run(seqlens, n_q=n_q, h_q=h_q, c=c)
+
+
+@pytest.mark.parametrize("c,h_q", [(64, 4), (128, 8)], ids=["c64", "c128_gqa4"])
+def test_batch_of_70_requests_spans_three_launch_groups(c, h_q):
+    rng = np.random.default_rng(7)
+    seqlens = [int(x) for x in rng.integers(1, 500, size=70)]
+    n_q = [max(1, int(n * f)) for n, f in zip(seqlens, rng.uniform(0.3, 1.0, size=70))]
+    _run(seqlens, n_q=n_q, h_q=h_q, c=c)
+
+
+def test_paged_batch_of_40_requests_gqa5():
+    # the paged workload's shape (GQA 5, head dim 128, 16-token pages) over
+    # two launch groups of request descriptors
+    rng = np.random.default_rng(8)
+    seqlens = [int(x) for x in rng.integers(1, 700, size=40)]
+    _run(seqlens, h_q=10, h_kv=2, c=128, page_size=16)
