@@ -853,6 +853,14 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   constexpr int NW = M * QB, NT = 64 * NW;
   // GQA 2: ping-pong between the two heads' waves (one of each per SIMD)
   constexpr bool PP = M == 2;
+  // Five waves, list-driven: a thread stages 7 K chunks and 4 V units of a
+  // tile (60 VGPRs).  Held together across the softmax they push the sparse
+  // kernel past 256 VGPRs (65 spilled), so the two sets take turns: V(i) is
+  // fetched at the end of iteration i - 1 and stored halfway through the QK
+  // MFMAs of iteration i, K(i + 1) is fetched right after those stores and
+  // stored after the softmax of iteration i.  The dense kernel fits with
+  // both sets held and keeps the common schedule.
+  constexpr bool ALT = !PP && !DENSE && M * q16_blocks(M) == 5;
   constexpr int KROW = C + 8, VROW = TILE + 8;
   constexpr int K_SLOT = TILE * KROW, V_SLOT = C * VROW;
   constexpr int K_CHUNKS = TILE * C / 8, V_UNITS = (TILE / 2) * (C / 8);
@@ -1157,6 +1165,68 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       };
       if (__builtin_amdgcn_readfirstlane(wave) < 4) run(YES);
       else run(NO);
+    }
+  } else if constexpr (ALT) {
+    if (n_tiles > 0) {
+      // entering iteration i: K(i) is in K slot i & 1 and V(i - 1) in V slot
+      // (i - 1) & 1; sv holds V(i), sk nothing; kt[j] is tile i + j and at1
+      // locates tile i + 1
+      KSet sk;
+      VSet sv;
+      int kt[2];
+      kt[0] = tile_or_none(0);
+      kt[1] = tile_or_none(1);
+      TileAt at1 = locate(kt[0]);
+      load_k_at(at1, sk);
+  #pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
+      load_v_at(at1, sv);
+      at1 = locate(kt[1]);
+      __syncthreads();
+      // iteration i (parity ip): PV(i - 1) from V slot 1 - ip and QK(i) from
+      // K slot ip; V(i) goes into V slot ip, K(i + 1) into K slot 1 - ip
+      auto iteration = [&](auto ipc, auto pv, auto qk, int i) INLINE {
+        constexpr int ip = decltype(ipc)::value;
+        constexpr bool QK = decltype(qk)::value;
+        constexpr int N = (decltype(pv)::value ? 2 * NCB : 0) + 4 * NKC;
+        constexpr int S0 = N / 2;
+        static_assert(S0 + 2 * VU_PER_T < N, "staging must fit between the MFMAs");
+        auto stage_hook = [&](auto jc) INLINE {
+          constexpr int j = decltype(jc)::value;
+          if constexpr (QK) {
+            if constexpr (j >= S0 && j < S0 + 2 * VU_PER_T && (j - S0) % 2 == 0)
+              store_v(ip, sv, (j - S0) / 2);
+            if constexpr (j == S0 + 2 * VU_PER_T) load_k_at(at1, sk);
+          }
+        };
+        stream(pv, qk, 1 - ip, ip, stage_hook);
+        if constexpr (QK) {
+          softmax(kt[0]);
+          __builtin_amdgcn_sched_barrier(0);
+  #pragma unroll
+          for (int u = 0; u < KC_PER_T; ++u) store_k(1 - ip, sk, u);
+          __builtin_amdgcn_sched_barrier(0);
+          load_v_at(at1, sv);
+          kt[0] = kt[1];
+          kt[1] = tile_or_none(i + 2);
+          at1 = locate(kt[1]);
+          __syncthreads();
+        }
+      };
+      const std::integral_constant<int, 0> P0;
+      const std::integral_constant<int, 1> P1;
+      iteration(P0, NO, YES, 0);
+      int it = 1;
+      for (; it + 1 < n_tiles; it += 2) {
+        iteration(P1, YES, YES, it);
+        iteration(P0, YES, YES, it + 1);
+      }
+      if (it < n_tiles) {
+        iteration(P1, YES, YES, it);
+        iteration(P0, YES, NO, it + 1);
+      } else {
+        iteration(P1, YES, NO, it);
+      }
     }
   } else {
     if (n_tiles > 0) {
