@@ -121,3 +121,36 @@ def _paged_case(c, m, page_size):
     want, want_lse = O.attention(q, k, v, 64, alpha)
     compare_outputs(pb.o_of(0), want, f"paged dense C={c} m={m}")
     _check_lse(lse.cpu().numpy(), want_lse)
+
+
+# Long rows: the steady state of each schedule's tile loop (both tile
+# parities, many iterations) on lists up to 40 tiles long, contiguous and
+# paged; the five-wave head-dim-256 kernel stages K and V in turns.
+LONG_N = 2500
+LONG_CASES = [(256, 5, False), (256, 5, True), (256, 2, False), (256, 3, True), (128, 4, False),
+              (128, 5, True), (64, 8, False)]
+
+
+@pytest.mark.parametrize("c,m,paged", LONG_CASES,
+                         ids=[f"c{c}_m{m}_{'paged' if p else 'contig'}" for c, m, p in LONG_CASES])
+def test_sparse_long_rows(c, m, paged):
+    wl = synth.workload("tiny_2k", h_q=2 * m, h_kv=2, head_dim=c, seed=300 + c + m)
+    seqs = synth.make_inputs(wl, seqlens=[LONG_N])
+    kw, prm = _params()
+    s = seqs[0]
+    q, k, v = s.q.double().numpy(), s.k.double().numpy(), s.v.double().numpy()
+    alpha = O.default_scale(c)
+    mask = O.estimate_mask(q, k, kw["block"], kw["group"], kw["gamma"], alpha)["mask"]
+    rp, cols, _ = O.expand_rescue([mask], [LONG_N], [LONG_N], kw["block"], kw["tile"],
+                                  kw["n_local"], kw["n_sink"], kw["eta"], kw["rho"], kw["seed"])
+    assert np.diff(rp).max() >= 20
+    drp, dcols = lists_to_device(rp, cols)
+    b = PagedBatch(seqs, [LONG_N], page_size=16, seed=11) if paged else DeviceBatch(seqs, None)
+    lg = Guarded(2 * m * LONG_N, torch.float32, fill=float("nan"))
+    bfla.bfla_sparse_prefill(b.prob, prm, b.qv, b.kv, drp, dcols, b.ov, lg.t)
+    torch.cuda.synchronize()
+    lg.check("long-row lse")
+    b.o_guard.check("long-row O")
+    want, want_lse = O.attention(q, k, v, 64, alpha, rp, cols, 0)
+    compare_outputs(b.o_of(0), want, f"long rows C={c} m={m} paged={paged}")
+    _check_lse(lg.t.cpu().numpy(), want_lse)
