@@ -162,3 +162,13 @@ def test_dual_stage_error_bound_holds():
     lhs = np.linalg.norm(o[0] - o_s[0])
     assert lhs > 0
     assert lhs <= alpha * np.linalg.norm(a) * np.linalg.norm(v[0])
+
+
+def test_default_scale_is_the_library_default():
+    # alpha = 1/sqrt(C) (eq15, eq27) is also scaled-dot-product attention's
+    # default scale: the oracle with its default equals the library without one
+    q, k, v = _qkv(21, 2, 2, 48, 48, 16)
+    o, _ = O.attention(q, k, v, 16, O.default_scale(16))
+    ref = F.scaled_dot_product_attention(torch.from_numpy(q), torch.from_numpy(k),
+                                         torch.from_numpy(v), is_causal=True).numpy()
+    np.testing.assert_allclose(o, ref, rtol=1e-10, atol=1e-12)

@@ -214,3 +214,74 @@ def test_gqa_union_contains_every_head_and_m1_is_identity():
     assert np.array_equal(st1["mask"].astype(bool), st1["head_keep"])
     # the diagonal block always enters the softmax and rows are never empty
     assert np.all(st_["head_keep"].sum(axis=-1) >= 1)
+
+
+def test_padded_groups_never_win_the_max_when_every_real_pair_is_negative():
+    # n = 192 with b = 128, g = 64: the last block holds one real group and
+    # one group that starts at n (all padding); every real group pair scores
+    # -g*C, so a padded group's zero dot product must not enter the max
+    c, b, g, n = 4, 128, 64, 192
+    q, k = np.ones((n, c)), -np.ones((n, c))
+    s = O.block_scores(q, k, b, g)
+    assert np.isfinite(s).sum() == 3
+    assert np.all(s[np.isfinite(s)] == -g * c)
+    # the same with a chunked prefix: 64 queries after 128 keys
+    s = O.block_scores(q[:64], k, b, g)
+    assert np.all(s[np.isfinite(s)] == -g * c)
+
+
+def test_unreached_threshold_keeps_every_block():
+    # the float32 masses of this row add up to 0.99999994 in keep order; a
+    # gamma below 1 whose float32 rounding is 1 is never reached, and then
+    # every causal block is kept (eq17 has no shorter prefix)
+    s = np.array([[-1.3, 0.7, -np.inf]], np.float32)
+    a = O.block_probs(s, 1.0)
+    assert np.float32(a[0, 1]) + np.float32(a[0, 0]) < np.float32(1.0)
+    gamma = 1.0 - 2.0 ** -26
+    assert gamma < 1.0 and np.float32(gamma) == np.float32(1.0)
+    keep, _, r = O.keep_mass(s, gamma, 1.0)
+    assert r[0] == 2 and keep[0].tolist() == [True, True, False]
+
+
+def test_gamma_is_compared_in_float32():
+    # reading R16: the running mass and gamma are both float32; a gamma a
+    # hair above the first block's float32 mass (same float32 value) is
+    # reached by that block alone, while a float64 comparison would take two
+    s = np.array([[-1.3, 0.7]], np.float32)
+    a0 = float(O.block_probs(s, 1.0)[0, 1])
+    gamma = a0 + 1e-9
+    assert np.float32(gamma) == np.float32(a0) and gamma > a0
+    _, _, r = O.keep_mass(s, gamma, 1.0)
+    assert r[0] == 1
+
+
+def test_threshold_tie_band_is_one_part_in_1e5():
+    # two blocks, alpha = 1: the mass before the second block is a0; gamma a
+    # relative 3e-6 above a0 puts the second block inside the near-tie band,
+    # 3e-5 above leaves it a sure keep
+    s = np.array([[1.0, 0.0]], np.float32)
+    a0 = float(O.block_probs(s, 1.0)[0, 0])
+    _, tie, r = O.keep_mass(s, a0 * (1 + 3e-6), 1.0)
+    assert r[0] == 2 and tie[0, 1]
+    _, tie, r = O.keep_mass(s, a0 * (1 + 3e-5), 1.0)
+    assert r[0] == 2 and not tie[0].any()
+
+
+def test_a_cell_kept_only_as_a_near_tie_is_not_sure():
+    # b = g = 1, C = 1: block scores are q_i * k_j.  Query 3 of head 0 scores
+    # [5, 3, 3, 0]: at gamma 0.85 it keeps block 0 and, of the two equal 3s,
+    # block 1 (index order); head 1 scores [-5, -3, -3, 0] and keeps block 3
+    # alone.  Block 1 of the union is kept only through an order tie: the
+    # smallest change to k[2] moves it to block 2, so neither is sure.
+    q = np.array([[[1.0], [1.0], [1.0], [1.0]], [[-1.0], [-1.0], [-1.0], [-1.0]]])
+    k = np.array([[[5.0], [3.0], [3.0], [0.0]]])
+    st_ = O.estimate_mask(q, k, 1, 1, 0.85, 1.0)
+    assert st_["mask"][0, 3].tolist() == [1, 1, 0, 1]
+    assert st_["status"][0, 3].tolist() == [O.KEEP_SURE, O.TIE, O.TIE, O.KEEP_SURE]
+    k2 = k.copy()
+    k2[0, 2, 0] = 3.0 * (1 + 1e-6)
+    st2 = O.estimate_mask(q, k2, 1, 1, 0.85, 1.0)
+    assert st2["mask"][0, 3].tolist() == [1, 0, 1, 1]
+    # every sure cell of the first call keeps its decision under the change
+    sure = st_["status"] != O.TIE
+    assert np.array_equal(st_["mask"][sure], st2["mask"][sure])
