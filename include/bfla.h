@@ -196,9 +196,10 @@ int bfla_list_capacity(const bfla_problem* prob, const bfla_params* params,
  *                  partial sums are needed (NULL / 0 is enough when there
  *                  are none).
  * Errors: INVALID_ARG, UNSUPPORTED (also: m > 8; more than 65536 KV blocks
- * per request; q rows of 128 * g consecutive tokens spanning 2 GiB or more,
- * i.e. (128 g - 1) * stride_tok + head_dim >= 2^30; paged K where 128 g
- * tokens may span more than 2048 pages), WORKSPACE, HIP. */
+ * per request; q rows of 256 * g consecutive tokens spanning 2 GiB or more,
+ * i.e. (256 g - 1) * stride_tok + head_dim >= 2^30; paged K where
+ * ceil(128 g / page_size) + 1 exceeds 2056 pages, e.g. g = 512 with 16-token
+ * pages), WORKSPACE, HIP. */
 int bfla_estimate_mask(const bfla_problem* prob, const bfla_params* params,
                        const bfla_view* q, const bfla_kv* kv,
                        uint8_t* block_mask, float* dbg_scores,

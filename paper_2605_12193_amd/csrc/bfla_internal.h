@@ -17,7 +17,7 @@ namespace bfla {
 constexpr int kScoreTileM = 256;
 constexpr int kScoreTileN = 128;
 constexpr int kScoreChunk = 64;
-constexpr int kScorePagesMax = 2048;
+constexpr int kScorePagesMax = 2056;
 // stages per inner accumulation chain of the score GEMM (summed into a
 // second accumulator; a split of the inner dimension cuts between chains)
 constexpr int kScoreChain = 8;

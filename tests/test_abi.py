@@ -198,7 +198,7 @@ def test_estimate_address_limits():
     addr = C.c_void_p(1 << 20)
     p, prm = _prob(), bfla.params()
     _, kv = _fake_views()
-    # q rows of one score tile (128 groups of 64 tokens) spanning >= 2 GiB
+    # q rows of one score tile (256 groups of 64 tokens) spanning >= 2 GiB
     wide = bfla.bfla_view(1 << 20, None, 0, 64, 1 << 18)
     st = L.bfla_estimate_mask(C.byref(p.c), C.byref(prm), C.byref(wide), C.byref(kv), addr,
                               addr, None, None, 0, None)

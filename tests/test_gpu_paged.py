@@ -92,3 +92,30 @@ def test_paged_dense_equals_contiguous():
         want, _ = O.attention(s.q.double().numpy(), s.k.double().numpy(), s.v.double().numpy(),
                               64, alpha)
         compare_outputs(pb.o_of(r), want, f"paged dense request {r}")
+
+
+def test_paged_stage1_with_wide_groups():
+    # b = g = 256 over 16-token pages: one score tile's keys (128 groups of
+    # 256 tokens) span 2048 pages, the most the paged score kernel resolves
+    # for the paper's widest group; masks and scores equal the contiguous
+    # run bit for bit and the oracle on sure cells
+    n, h_q, h_kv, c = 33000, 2, 1, 64
+    wl = synth.workload("paged_4x", seqlens=[n], h_q=h_q, h_kv=h_kv, head_dim=c)
+    seqs = synth.make_inputs(wl)
+    pb = PagedBatch(seqs, [n], 16, wl.seed)
+    db = DeviceBatch(seqs, [n])
+    prm = bfla.params(block=256, group=256, gamma=0.95)
+    got = []
+    for b in (pb, db):
+        buf = bfla.Buffers(b.prob, prm)
+        bfla.bfla_estimate_mask(b.prob, prm, b.qv, b.kv, buf.block_mask, dbg_scores=buf.scores,
+                                workspace=buf.ws_estimate)
+        torch.cuda.synchronize()
+        got.append((buf.block_mask.cpu().numpy(), buf.scores.cpu().numpy()))
+    assert np.array_equal(got[0][0], got[1][0])
+    assert np.array_equal(got[0][1], got[1][1], equal_nan=True)
+    s = seqs[0]
+    st = O.estimate_mask(s.q.double().numpy(), s.k.double().numpy(), 256, 256, 0.95,
+                         O.default_scale(c))
+    mask_compare(got[0][0][:st["mask"].size].reshape(st["mask"].shape), st["mask"],
+                 st["status"])

@@ -7,6 +7,8 @@ contiguous or paged K/V (page sizes 16-64).  Bars as everywhere: block mask
 exact on sure cells, lists bit-exact against the oracle's tile stage on the
 GPU mask, sparse and dense outputs within max-abs 2e-2 / rel-L2 5e-3, LSE
 within 2e-4."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -18,7 +20,8 @@ from parity_util import (DeviceBatch, Guarded, GuardedBuffers, PagedBatch, compa
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 48
+# more cases on request (same seeds first): BFLA_RANDOM_CASES=400 pytest ...
+N_CASES = int(os.environ.get("BFLA_RANDOM_CASES", "48"))
 
 
 def draw(i):
