@@ -9,11 +9,18 @@ local-band and rescue rules (eq19-eq26), and exact attention restricted to
 the retained tiles (eq27).  N_q < N_kv is a chunked prefill: the queries are
 the last N_q positions of the sequence.
 
+Two more layouts take variable-length batches: `forward_varlen` (packed
+token-major Q [sum N_q, H_q, C] and K, V [sum N_kv, H_kv, C] with cumulative
+sequence lengths, as flash-attention's varlen interface) and `forward_paged`
+(packed Q with K, V in page pools [pages, page_size, H_kv, C] addressed
+through an int32 block table, as vLLM's cache).  Request r's queries are the
+last N_q(r) positions of its N_kv(r) keys.
+
 Every step runs in the library's HIP kernels, enqueued on the current torch
 stream; this module only checks shapes, keeps the device buffers of the last
 shape and passes pointers.
 """
-from typing import Optional, Tuple
+from typing import List, Optional, Sequence, Tuple
 
 import torch
 
@@ -48,6 +55,73 @@ def _layout(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor):
     return batch, h_q, h_kv, n_q, n_kv, c
 
 
+def _host_ints(x, name: str) -> List[int]:
+    """Lengths size the launch, so they are read on the host: a sequence or a
+    CPU tensor (a GPU tensor would force a synchronisation here)."""
+    if isinstance(x, torch.Tensor):
+        if x.is_cuda:
+            raise ValueError(f"{name} must be a host sequence or CPU tensor")
+        x = x.tolist()
+    return [int(e) for e in x]
+
+
+def _lengths(cu: Sequence[int], total: int, name: str) -> List[int]:
+    if len(cu) < 2 or cu[0] != 0 or cu[-1] != total:
+        raise ValueError(f"{name} must start at 0 and end at {total}, got {list(cu)}")
+    n = [b - a for a, b in zip(cu[:-1], cu[1:])]
+    if min(n) < 1:
+        raise ValueError(f"{name} holds an empty or negative length: {n}")
+    return n
+
+
+def _packed(name: str, t: torch.Tensor) -> None:
+    if t.dim() != 3 or t.dtype != torch.bfloat16 or not t.is_cuda or t.stride(-1) != 1:
+        raise ValueError(f"{name} must be a bf16 [tokens, heads, C] GPU tensor with a "
+                         "contiguous last dimension")
+
+
+def _varlen_layout(q, n_q: Sequence[int], n_kv: Sequence[int], h_kv: int, c_k: int):
+    _packed("q", q)
+    _, h_q, c = q.shape
+    if c_k != c:
+        raise ValueError(f"q and k disagree on head_dim ({c} vs {c_k})")
+    if h_q % h_kv:
+        raise ValueError(f"H_q = {h_q} is not a multiple of H_kv = {h_kv}")
+    if len(n_q) != len(n_kv):
+        raise ValueError(f"{len(n_q)} query lengths for {len(n_kv)} key lengths")
+    for r, (a, b) in enumerate(zip(n_q, n_kv)):
+        if a > b:
+            raise ValueError(f"request {r}: N_q = {a} > N_kv = {b}")
+    return h_q, c
+
+
+class _Pass:
+    """The buffers of one (lengths, heads, C, device) shape, kept between calls."""
+
+    def __init__(self):
+        self.key = None
+        self.prob: Optional[bfla.Problem] = None
+        self.buf: Optional[bfla.Buffers] = None
+
+    def get(self, prm, n_q, n_kv, h_q, h_kv, c, device):
+        key = (tuple(n_q), tuple(n_kv), h_q, h_kv, c, device)
+        if key != self.key:
+            self.prob = bfla.Problem(list(n_q), list(n_kv), h_q, h_kv, c)
+            self.buf = bfla.Buffers(self.prob, prm, device=device)
+            self.key = key
+        return self.prob, self.buf
+
+
+def _lse_views(lse: torch.Tensor, h_q: int, n_q: Sequence[int]) -> Tuple[torch.Tensor, ...]:
+    """Per-request [H_q, N_q(r)] views of the library's LSE (request r after
+    the H_q * N_q of the requests before it)."""
+    out, off = [], 0
+    for n in n_q:
+        out.append(lse[off:off + h_q * n].view(h_q, n))
+        off += h_q * n
+    return tuple(out)
+
+
 class BlockFilteredAttention(torch.nn.Module):
     """Sparse causal prefill attention with BFLA's block filter.
 
@@ -69,6 +143,7 @@ class BlockFilteredAttention(torch.nn.Module):
         self._key = None
         self._buf: Optional[bfla.Buffers] = None
         self._prob: Optional[bfla.Problem] = None
+        self._varlen, self._paged = _Pass(), _Pass()
 
     def _pass_buffers(self, batch, h_q, h_kv, n_q, n_kv, c, device):
         key = (batch, h_q, h_kv, n_q, n_kv, c, device)
@@ -88,6 +163,51 @@ class BlockFilteredAttention(torch.nn.Module):
             return o
         lse = buf.lse.view(batch, h_q, n_q).clone()
         return o, (lse if q.dim() == 4 else lse[0])
+
+    def forward_varlen(self, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                       cu_seqlens_q, cu_seqlens_k):
+        """Packed variable-length batch: q [sum N_q, H_q, C], k / v [sum N_kv,
+        H_kv, C] (same strides), cu_seqlens_* the cumulative lengths (host ints,
+        B + 1 of them, from 0).  Returns O like q (and, with return_lse, one
+        [H_q, N_q(r)] LSE view per request)."""
+        _packed("k", k)
+        if v.shape != k.shape or v.stride() != k.stride():
+            raise ValueError("v must have k's shape and strides")
+        cq = _host_ints(cu_seqlens_q, "cu_seqlens_q")
+        ck = _host_ints(cu_seqlens_k, "cu_seqlens_k")
+        n_q = _lengths(cq, q.shape[0], "cu_seqlens_q")
+        n_kv = _lengths(ck, k.shape[0], "cu_seqlens_k")
+        h_q, c = _varlen_layout(q, n_q, n_kv, k.shape[1], k.shape[2])
+        prob, buf = self._varlen.get(self.prm, n_q, n_kv, h_q, k.shape[1], c, q.device)
+        o = torch.empty_like(q)
+        kv = bfla.KV(k.transpose(0, 1), v.transpose(0, 1),
+                     batch_offsets=[s * k.stride(0) for s in ck[:-1]])
+        bfla.sparse_pass(prob, self.prm, bfla.view_packed(q, cq[:-1]), kv,
+                         bfla.view_packed(o, cq[:-1]), buf)
+        return (o, _lse_views(buf.lse, h_q, n_q)) if self.return_lse else o
+
+    def forward_paged(self, q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                      block_table: torch.Tensor, seqlens_k, cu_seqlens_q):
+        """Packed queries over a paged cache: q [sum N_q, H_q, C]; k_cache /
+        v_cache [pages, page_size, H_kv, C] (same strides, page_size a power of
+        two >= 16); block_table int32 [B, max_pages] on the GPU, row r listing
+        request r's pages in order; seqlens_k the N_kv(r) and cu_seqlens_q the
+        cumulative query lengths (host ints).  Returns O like q (and the LSE
+        views with return_lse)."""
+        if k_cache.dim() != 4 or k_cache.dtype != torch.bfloat16 or not k_cache.is_cuda:
+            raise ValueError("k_cache must be a bf16 [pages, page_size, H_kv, C] GPU tensor")
+        cq = _host_ints(cu_seqlens_q, "cu_seqlens_q")
+        n_q = _lengths(cq, q.shape[0], "cu_seqlens_q")
+        n_kv = _host_ints(seqlens_k, "seqlens_k")
+        if block_table.dim() != 2 or block_table.shape[0] != len(n_kv):
+            raise ValueError(f"block_table needs one row per request ({len(n_kv)})")
+        h_q, c = _varlen_layout(q, n_q, n_kv, k_cache.shape[2], k_cache.shape[3])
+        prob, buf = self._paged.get(self.prm, n_q, n_kv, h_q, k_cache.shape[2], c, q.device)
+        o = torch.empty_like(q)
+        kv = bfla.KV(k_cache, v_cache, paged=True, block_table=block_table)
+        bfla.sparse_pass(prob, self.prm, bfla.view_packed(q, cq[:-1]), kv,
+                         bfla.view_packed(o, cq[:-1]), buf)
+        return (o, _lse_views(buf.lse, h_q, n_q)) if self.return_lse else o
 
 
 def block_filtered_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, **kw):

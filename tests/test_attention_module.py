@@ -49,3 +49,21 @@ def test_kv_descriptor_checks():
                   None):
         with pytest.raises(ValueError, match="block_table"):
             bfla.KV(pages, pages, paged=True, block_table=table)
+
+
+def test_varlen_length_rules():
+    from paper_2605_12193_amd.attention import _host_ints, _lengths
+    assert _lengths([0, 3, 10], 10, "cu") == [3, 7]
+    assert _host_ints(torch.tensor([0, 5]), "cu") == [0, 5]
+    for cu, total in (([1, 3], 3), ([0, 3], 4), ([0, 3, 3], 3), ([0], 0)):
+        with pytest.raises(ValueError, match="cu"):
+            _lengths(cu, total, "cu")
+
+
+def test_varlen_and_paged_reject_host_tensors():
+    q = _t(10, 4, 64)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        BlockFilteredAttention().forward_varlen(q, _t(10, 2, 64), _t(10, 2, 64), [0, 10], [0, 10])
+    with pytest.raises(ValueError, match="GPU tensor"):
+        BlockFilteredAttention().forward_paged(q, _t(4, 16, 2, 64), _t(4, 16, 2, 64),
+                                               torch.zeros(1, 4, dtype=torch.int32), [10], [0, 10])

@@ -1,6 +1,7 @@
 """The PyTorch drop-in on the GPU: outputs against the oracle, an all-keep
 configuration equal to the dense kernel bit for bit, buffer reuse and a
-chunked call."""
+chunked call; the packed variable-length entry against the head-first
+library run and the oracle, and the paged-cache entry against it."""
 import numpy as np
 import pytest
 import torch
@@ -8,7 +9,7 @@ import torch
 from oracle import bfla_oracle as O
 from paper_2605_12193_amd import bfla, synth
 from paper_2605_12193_amd.attention import BlockFilteredAttention
-from parity_util import compare_outputs
+from parity_util import DeviceBatch, PagedBatch, compare_outputs
 
 pytestmark = pytest.mark.gpu
 
@@ -84,3 +85,66 @@ def test_buffers_reused_and_chunked_call():
     rp, cols, _ = O.expand_rescue([mask], [300], [1200], 128, 64, 2, 1, 16, 0.0, 0)
     want, _ = O.attention(qh, kh, vh, 64, alpha, rp, cols, 0)
     compare_outputs(oc[0].float().cpu().numpy(), want, "chunked")
+
+
+def _packed_requests(n_kv, n_q, h_q, h_kv, c):
+    wl = synth.workload("paged_4x", seqlens=n_kv, h_q=h_q, h_kv=h_kv, head_dim=c)
+    seqs = synth.make_inputs(wl)
+    q = torch.cat([s.q[:, s.q.shape[1] - nq:].transpose(0, 1) for s, nq in zip(seqs, n_q)])
+    k = torch.cat([s.k.transpose(0, 1) for s in seqs])
+    v = torch.cat([s.v.transpose(0, 1) for s in seqs])
+    cu_q = np.concatenate([[0], np.cumsum(n_q)]).tolist()
+    cu_k = np.concatenate([[0], np.cumsum(n_kv)]).tolist()
+    return seqs, q.contiguous().cuda(), k.contiguous().cuda(), v.contiguous().cuda(), cu_q, cu_k
+
+
+VARLEN = ([700, 1500, 900], [700, 1500, 200], 8, 2, 128)   # the third request is chunked
+
+
+def test_varlen_matches_head_first_batch_and_oracle():
+    n_kv, n_q, h_q, h_kv, c = VARLEN
+    seqs, q, k, v, cu_q, cu_k = _packed_requests(n_kv, n_q, h_q, h_kv, c)
+    att = BlockFilteredAttention(gamma=0.9, rho=0.1, seed=3, return_lse=True)
+    o, lses = att.forward_varlen(q, k, v, cu_q, cu_k)
+    torch.cuda.synchronize()
+    assert o.shape == q.shape and len(lses) == 3
+    # the same requests head-first through the library: bit for bit
+    db = DeviceBatch(seqs, n_q)
+    prm = bfla.params(gamma=0.9, rho=0.1, seed=3)
+    buf = bfla.Buffers(db.prob, prm)
+    bfla.sparse_pass(db.prob, prm, db.qv, db.kv, db.ov, buf)
+    torch.cuda.synchronize()
+    assert torch.equal(att._varlen.buf.block_mask, buf.block_mask)
+    for r in range(3):
+        got = o[cu_q[r]:cu_q[r + 1]].transpose(0, 1).float().cpu().numpy()
+        assert np.array_equal(got, db.o_of(r))
+    # and the oracle on the module's own mask
+    mask = att._varlen.buf.block_mask.cpu().numpy()
+    alpha, off, masks = O.default_scale(c), 0, []
+    for r, s in enumerate(seqs):
+        lq, lkv = -(-n_q[r] // 128), -(-n_kv[r] // 128)
+        masks.append(mask[off:off + h_kv * lq * lkv].reshape(h_kv, lq, lkv))
+        off += h_kv * lq * lkv
+    rp, cols, _ = O.expand_rescue(masks, n_q, n_kv, 128, 64, 2, 1, 16, 0.1, 3)
+    base = 0
+    for r, s in enumerate(seqs):
+        qh = s.q[:, n_kv[r] - n_q[r]:].double().numpy()
+        want, want_lse = O.attention(qh, s.k.double().numpy(), s.v.double().numpy(), 64, alpha,
+                                     rp, cols, base)
+        base += h_kv * -(-n_q[r] // 64)
+        got = o[cu_q[r]:cu_q[r + 1]].transpose(0, 1).float().cpu().numpy()
+        compare_outputs(got, want, f"varlen request {r}")
+        np.testing.assert_allclose(lses[r].cpu().numpy(), want_lse, rtol=0, atol=2e-4)
+
+
+def test_paged_cache_equals_varlen():
+    n_kv, n_q, h_q, h_kv, c = VARLEN
+    seqs, q, k, v, cu_q, cu_k = _packed_requests(n_kv, n_q, h_q, h_kv, c)
+    att = BlockFilteredAttention(gamma=0.9, rho=0.1, seed=3)
+    o_var = att.forward_varlen(q, k, v, cu_q, cu_k)
+    pb = PagedBatch(seqs, n_q, page_size=16, seed=5)
+    assert torch.equal(pb.q, q)
+    o_pg = att.forward_paged(pb.q, pb.kp, pb.vp, pb.table, n_kv, torch.tensor(cu_q))
+    o_again = att.forward_paged(pb.q, pb.kp, pb.vp, pb.table, n_kv, cu_q)
+    torch.cuda.synchronize()
+    assert torch.equal(o_pg, o_var) and torch.equal(o_again, o_pg)
