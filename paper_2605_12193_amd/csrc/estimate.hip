@@ -463,6 +463,71 @@ __device__ __forceinline__ bool better(float s1, int j1, float s2, int j2) {
   return s1 > s2 || (s1 == s2 && j1 < j2);
 }
 
+// Wave-wide reductions without LDS round trips.  Step k hands every lane
+// the partial result of a partner lane in another group of 2^k lanes:
+// lane ^ 1 and lane ^ 2 (DPP quad permutations), the lane mirrored in its
+// 8 and in its 16 (DPP row_half_mirror, row_mirror), then lane ^ 16 and
+// lane ^ 32 (v_permlane16_swap / v_permlane32_swap, which deliver both
+// lanes of the pair).  Partners hold the same set of lanes, and a + b ==
+// b + a exactly, so every lane ends with the bit-identical result.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, false);
+}
+constexpr int DPP_XOR1 = 0xB1, DPP_XOR2 = 0x4E, DPP_HALF_MIRROR = 0x141, DPP_MIRROR = 0x140;
+
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t x, Op op) {
+  x = op(x, dpp_u32<DPP_XOR1>(x));
+  x = op(x, dpp_u32<DPP_XOR2>(x));
+  x = op(x, dpp_u32<DPP_HALF_MIRROR>(x));
+  x = op(x, dpp_u32<DPP_MIRROR>(x));
+  const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = op((uint32_t)p[0], (uint32_t)p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return op((uint32_t)q[0], (uint32_t)q[1]);
+}
+__device__ __forceinline__ float wave_max(float x) {
+  return __builtin_bit_cast(float, wave_reduce_u32(__builtin_bit_cast(uint32_t, x),
+      [](uint32_t a, uint32_t b) {
+        return __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a),
+                                                  __builtin_bit_cast(float, b)));
+      }));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  return __builtin_bit_cast(float, wave_reduce_u32(__builtin_bit_cast(uint32_t, x),
+      [](uint32_t a, uint32_t b) {
+        return __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) +
+                                                __builtin_bit_cast(float, b));
+      }));
+}
+// (score, block) pair that ranks first under better(), in every lane
+__device__ __forceinline__ void wave_best(float& s, int& j) {
+  auto step = [&](float os, int oj) {
+    if (better(os, oj, s, j)) { s = os; j = oj; }
+  };
+  auto sw = [](float x) { return __builtin_bit_cast(uint32_t, x); };
+  auto fl = [](uint32_t x) { return __builtin_bit_cast(float, x); };
+  step(fl(dpp_u32<DPP_XOR1>(sw(s))), (int)dpp_u32<DPP_XOR1>((uint32_t)j));
+  step(fl(dpp_u32<DPP_XOR2>(sw(s))), (int)dpp_u32<DPP_XOR2>((uint32_t)j));
+  step(fl(dpp_u32<DPP_HALF_MIRROR>(sw(s))), (int)dpp_u32<DPP_HALF_MIRROR>((uint32_t)j));
+  step(fl(dpp_u32<DPP_MIRROR>(sw(s))), (int)dpp_u32<DPP_MIRROR>((uint32_t)j));
+  {
+    const auto ps = __builtin_amdgcn_permlane16_swap(sw(s), sw(s), false, false);
+    const auto pj = __builtin_amdgcn_permlane16_swap((uint32_t)j, (uint32_t)j, false, false);
+    s = fl((uint32_t)ps[0]);
+    j = (int)pj[0];
+    step(fl((uint32_t)ps[1]), (int)pj[1]);
+  }
+  {
+    const auto ps = __builtin_amdgcn_permlane32_swap(sw(s), sw(s), false, false);
+    const auto pj = __builtin_amdgcn_permlane32_swap((uint32_t)j, (uint32_t)j, false, false);
+    s = fl((uint32_t)ps[0]);
+    j = (int)pj[0];
+    step(fl((uint32_t)ps[1]), (int)pj[1]);
+  }
+}
+
 __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
   __shared__ uint32_t keep_bits[MAX_LKV / 32];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -518,10 +583,10 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
     // softmax statistics (eq15)
     float mx = -INFINITY;
     for_each([&](int, float s) { mx = fmaxf(mx, s); });
-    for (int d = 32; d >= 1; d >>= 1) mx = fmaxf(mx, __shfl_xor(mx, d));
+    mx = wave_max(mx);
     float z = 0.f;
     for_each([&](int, float s) { z += expf(a.alpha * (s - mx)); });
-    for (int d = 32; d >= 1; d >>= 1) z += __shfl_xor(z, d);
+    z = wave_sum(z);
 
     // keep-mass selection (eq16-eq18): repeated arg-max below the last pick
     float mass = 0.f;
@@ -533,11 +598,7 @@ __global__ void __launch_bounds__(512) select_kernel(SelectArgs a) {
       for_each([&](int j, float s) {
         if (better(s_prev, j_prev, s, j) && better(s, j, bs, bj)) { bs = s; bj = j; }
       });
-      for (int d = 32; d >= 1; d >>= 1) {
-        const float os = __shfl_xor(bs, d);
-        const int oj = __shfl_xor(bj, d);
-        if (better(os, oj, bs, bj)) { bs = os; bj = oj; }
-      }
+      wave_best(bs, bj);
       if (bj >= n_causal) break;  // only with non-finite scores: nothing left to rank
       if (lane == 0) {
         atomicOr(&keep_bits[bj >> 5], 1u << (bj & 31));
