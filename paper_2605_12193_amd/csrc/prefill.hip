@@ -704,9 +704,18 @@ prefill_kernel(PrefillArgs a) {
   }
 
   // ---- epilogue: O = O^T / l, LSE ----
-  if (!q_ok) return;
+  // A lane holds 4-channel pieces of one query row, so storing the O^T
+  // accumulators directly makes every store touch 32 rows.  Each wave
+  // instead writes its 32 x C block into LDS (the K/V stages are free once
+  // every wave has left the tile loop) and stores whole rows from there,
+  // 16 bytes per lane and C / 8 lanes per row.  A wave reads back only its
+  // own rows, which its LDS stores precede in order.
+  constexpr int OROW = C + 8;                    // bf16 row pitch of the staged block
+  constexpr int LDS_BYTES = (PP ? 3 : 2) * CF::STAGE * 2;
+  static_assert(Shape<C, M>::WAVES * 32 * OROW * 2 <= LDS_BYTES, "O staging exceeds the LDS");
   const float inv = (l_run > 0.f) ? 1.f / l_run : 0.f;
-  bf16_t* op = a.o + o_off + (int64_t)p * a.o_sh + (int64_t)t * a.o_st;
+  __syncthreads();
+  bf16_t* const ow = lds + wave * 32 * OROW;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
@@ -714,10 +723,22 @@ prefill_kernel(PrefillArgs a) {
       uint2 u;
       u.x = pack_bf16x2(acc[cb][4 * rg + 0] * inv, acc[cb][4 * rg + 1] * inv);
       u.y = pack_bf16x2(acc[cb][4 * rg + 2] * inv, acc[cb][4 * rg + 3] * inv);
-      *reinterpret_cast<uint2*>(op + 32 * cb + 8 * rg + 4 * hi) = u;
+      *reinterpret_cast<uint2*>(ow + l32 * OROW + 32 * cb + 8 * rg + 4 * hi) = u;
     }
   }
-  if (a.lse && hi == 0) {
+  {
+    constexpr int LPR = C / 8, RPI = 64 / LPR;   // lanes per row, rows per store
+    const int r0 = lane / LPR, ch = 8 * (lane % LPR);
+    const int t0 = qt * TILE + half * 32;
+    bf16_t* const ob = a.o + o_off + (int64_t)p * a.o_sh;
+#pragma unroll
+    for (int i = 0; i < 32 / RPI; ++i) {
+      const int r = r0 + RPI * i;
+      const uint4 u = *reinterpret_cast<const uint4*>(ow + r * OROW + ch);
+      if (t0 + r < n_q) *reinterpret_cast<uint4*>(ob + (int64_t)(t0 + r) * a.o_st + ch) = u;
+    }
+  }
+  if (a.lse && hi == 0 && q_ok) {
     float v = (l_run > 0.f) ? m_run * a.scale + logf(l_run) : -INFINITY;
     a.lse[lse_off + (int64_t)p * n_q + t] = v;
   }
@@ -1294,17 +1315,34 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
     }
   }
 
-  if (t >= n_q) return;
+  // O through LDS as in prefill_kernel: each wave stages its 16 x C block
+  // (the K/V rings are free once every wave has left the tile loop) and
+  // stores whole rows, 16 bytes per lane.
+  constexpr int OROW = C + 8;
+  constexpr int LDS_BYTES = (2 * TILE * (C + 8) + 2 * C * (TILE + 8)) * 2;
+  static_assert(NW * 16 * OROW * 2 <= LDS_BYTES, "O staging exceeds the LDS");
   const float inv = (l_run > 0.f) ? 1.f / l_run : 0.f;
-  bf16_t* op = a.o + o_off + (int64_t)p * a.o_sh + (int64_t)t * a.o_st + 4 * g;
+  __syncthreads();
+  bf16_t* const ow = lds + wave * 16 * OROW;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     uint2 u;
     u.x = pack_bf16x2(acc[cb][0] * inv, acc[cb][1] * inv);
     u.y = pack_bf16x2(acc[cb][2] * inv, acc[cb][3] * inv);
-    *reinterpret_cast<uint2*>(op + 16 * cb) = u;
+    *reinterpret_cast<uint2*>(ow + l16 * OROW + 16 * cb + 4 * g) = u;
   }
-  if (a.lse && g == 0) {
+  {
+    constexpr int LPR = C / 8, RPI = 64 / LPR;   // lanes per row, rows per store
+    const int r0 = lane / LPR, ch = 8 * (lane % LPR);
+    bf16_t* const ob = a.o + o_off + (int64_t)p * a.o_sh;
+#pragma unroll
+    for (int i = 0; i < 16 / RPI; ++i) {
+      const int r = r0 + RPI * i;
+      const uint4 u = *reinterpret_cast<const uint4*>(ow + r * OROW + ch);
+      if (q16 + r < n_q) *reinterpret_cast<uint4*>(ob + (int64_t)(q16 + r) * a.o_st + ch) = u;
+    }
+  }
+  if (a.lse && g == 0 && t < n_q) {
     float v = (l_run > 0.f) ? m_run * a.scale + logf(l_run) : -INFINITY;
     a.lse[lse_off + (int64_t)p * n_q + t] = v;
   }
