@@ -224,6 +224,22 @@ def test_llama_128k_sampled(llama_128k, gamma, rho):
           f"mismatches {ties}, max-abs {err[0]:.2e} rel-L2 {err[1]:.2e}", flush=True)
 
 
+def test_llama_128k_dense_sampled(llama_128k):
+    # the dense baseline at the headline size, in its launch configuration:
+    # sampled rows (early, middle, last q-tiles) against the oracle over every
+    # causal key
+    wl, c = llama_128k
+    m = wl.h_q // wl.h_kv
+    alpha = O.default_scale(wl.head_dim)
+    od = torch.empty_like(c.o)
+    bfla.bfla_dense_prefill(c.prob, bfla.params(**_kw(wl)), c.qv, c.kv, bfla.view_hnc(od))
+    torch.cuda.synchronize()
+    t_q = c.n // 64
+    rows = [(0, 0), (3, t_q // 3), (6, t_q // 2 + 7), (7, t_q - 1)]
+    get = lambda p, a, b: od[p, a:b].float().cpu().numpy()
+    check_rows_out(c.host, m, alpha, get, None, None, rows, "128K dense rows", dense=True)
+
+
 def test_paged_4x_per_request():
     wl = synth.workload("paged_4x")
     seqs = synth.make_inputs(wl)
