@@ -252,17 +252,26 @@ prefill_kernel(PrefillArgs a) {
 
   bf16x8 qf[NKC];
   {
-    const bf16_t* qp = a.q + q_off + (int64_t)p * a.q_sh + (int64_t)t * a.q_st + 8 * hi;
+    // whole rows through LDS: C / 8 lanes per row, 16 bytes per lane
+    constexpr int QROW = C + 8, LPR = C / 8, RPI = 64 / LPR;
+    bf16_t* const qs = lds + wave * 32 * QROW;
+    const int r0 = lane / LPR, ch = 8 * (lane % LPR);
+    const int t0 = qt * TILE + half * 32;
+    const bf16_t* const qb = a.q + q_off + (int64_t)p * a.q_sh;
+    uint4 v[32 / RPI];
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
-      uint4 v = q_ok ? ld16(qp + 16 * kc) : make_uint4(0, 0, 0, 0);
-      qf[kc] = as_bf16x8(v);
+    for (int i = 0; i < 32 / RPI; ++i) {
+      const int r = r0 + RPI * i;
+      v[i] = t0 + r < n_q ? ld16(qb + (int64_t)(t0 + r) * a.q_st + ch) : make_uint4(0, 0, 0, 0);
     }
+#pragma unroll
+    for (int i = 0; i < 32 / RPI; ++i)
+      *reinterpret_cast<uint4*>(qs + (r0 + RPI * i) * QROW + ch) = v[i];
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc)
+      qf[kc] = as_bf16x8(*reinterpret_cast<const uint4*>(qs + l32 * QROW + 16 * kc + 8 * hi));
   }
-  // Q must be resident before the loop: otherwise the waitcnt pass keeps the
-  // Q loads pending at the loop header and waits for every outstanding load
-  // (including the next tile's prefetch) on each iteration.
-  __builtin_amdgcn_s_waitcnt(VMCNT0);
+  __syncthreads();   // every wave holds its Q before the K/V stages are written
 
   // ---- K/V addressing ----
   // Contiguous: one descriptor per head spanning its N_kv rows.  Paged: one
