@@ -251,27 +251,29 @@ prefill_kernel(PrefillArgs a) {
   const int key_lim = min(q_pos, n_kv - 1);           // last admissible key
 
   bf16x8 qf[NKC];
+  constexpr int QROW = C + 8, QLPR = C / 8, QRPI = 64 / QLPR;
+  uint4 qv[32 / QRPI];
   {
-    // whole rows through LDS: C / 8 lanes per row, 16 bytes per lane
-    constexpr int QROW = C + 8, LPR = C / 8, RPI = 64 / LPR;
-    bf16_t* const qs = lds + wave * 32 * QROW;
-    const int r0 = lane / LPR, ch = 8 * (lane % LPR);
+    const int r0 = lane / QLPR, ch = 8 * (lane % QLPR);
     const int t0 = qt * TILE + half * 32;
     const bf16_t* const qb = a.q + q_off + (int64_t)p * a.q_sh;
-    uint4 v[32 / RPI];
 #pragma unroll
-    for (int i = 0; i < 32 / RPI; ++i) {
-      const int r = r0 + RPI * i;
-      v[i] = t0 + r < n_q ? ld16(qb + (int64_t)(t0 + r) * a.q_st + ch) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 32 / QRPI; ++i) {
+      const int r = r0 + QRPI * i;
+      qv[i] = t0 + r < n_q ? ld16(qb + (int64_t)(t0 + r) * a.q_st + ch) : make_uint4(0, 0, 0, 0);
     }
+  }
+  auto q_from_lds = [&]() INLINE {
+    bf16_t* const qs = lds + wave * 32 * QROW;
+    const int r0 = lane / QLPR, ch = 8 * (lane % QLPR);
 #pragma unroll
-    for (int i = 0; i < 32 / RPI; ++i)
-      *reinterpret_cast<uint4*>(qs + (r0 + RPI * i) * QROW + ch) = v[i];
+    for (int i = 0; i < 32 / QRPI; ++i)
+      *reinterpret_cast<uint4*>(qs + (r0 + QRPI * i) * QROW + ch) = qv[i];
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
       qf[kc] = as_bf16x8(*reinterpret_cast<const uint4*>(qs + l32 * QROW + 16 * kc + 8 * hi));
-  }
-  __syncthreads();   // every wave holds its Q before the K/V stages are written
+    __syncthreads();   // every wave holds its Q before the K/V stages are written
+  };
 
   // ---- K/V addressing ----
   // Contiguous: one descriptor per head spanning its N_kv rows.  Paged: one
@@ -596,6 +598,7 @@ prefill_kernel(PrefillArgs a) {
     // Past the end of the list the loads read zeros (no memory traffic) and
     // the stores fill a stage no one reads, so the loop body has no branches
     // around its memory operations.
+    if (n_tiles <= 0) q_from_lds();
     if (n_tiles > 0) {
       Staged sg0, sg1;
       int kt[5];  // tiles i .. i+4
@@ -603,6 +606,7 @@ prefill_kernel(PrefillArgs a) {
       for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
       load_tile(kt[0], sg0);
       load_tile(kt[1], sg1);
+      q_from_lds();
       store_tile(stage(0), sg0);
       store_tile(stage(1), sg1);
       load_tile(kt[2], sg0);
@@ -685,6 +689,7 @@ prefill_kernel(PrefillArgs a) {
     // tile i + 2 fetched, between the MFMAs of the PV stream of iteration i,
     // where the wave's VALU and LDS ports are otherwise idle.  Past the end of
     // the list the loads read zeros and the stores fill the unused stage.
+    q_from_lds();
     if (n_tiles > 0) {
       Staged sg;
       load_tile(tile_at(0), sg);
