@@ -250,6 +250,12 @@ prefill_kernel(PrefillArgs a) {
   const int wave_q0 = n_c + qt * TILE + half * 32;
   const int key_lim = min(q_pos, n_kv - 1);           // last admissible key
 
+  // Q is fetched as whole rows (C / 8 lanes per row, 16 bytes per lane; a
+  // lane's MFMA fragments are 16-byte pieces of one row, and loading those
+  // directly makes every load touch 32 rows), then redistributed through the
+  // still-empty K/V stages by q_from_lds().  The ping-pong prologue issues
+  // its first tile fetches before that call, so the Q and K/V round trips
+  // overlap.
   bf16x8 qf[NKC];
   constexpr int QROW = C + 8, QLPR = C / 8, QRPI = 64 / QLPR;
   uint4 qv[32 / QRPI];
