@@ -253,8 +253,8 @@ prefill_kernel(PrefillArgs a) {
   // Q is fetched as whole rows (C / 8 lanes per row, 16 bytes per lane; a
   // lane's MFMA fragments are 16-byte pieces of one row, and loading those
   // directly makes every load touch 32 rows), then redistributed through the
-  // still-empty K/V stages by q_from_lds().  The ping-pong prologue issues
-  // its first tile fetches before that call, so the Q and K/V round trips
+  // still-empty K/V stages by q_from_lds().  Both prologues issue their
+  // first tile fetches before that call, so the Q and K/V round trips
   // overlap.
   bf16x8 qf[NKC];
   constexpr int QROW = C + 8, QLPR = C / 8, QRPI = 64 / QLPR;
@@ -695,10 +695,11 @@ prefill_kernel(PrefillArgs a) {
     // tile i + 2 fetched, between the MFMAs of the PV stream of iteration i,
     // where the wave's VALU and LDS ports are otherwise idle.  Past the end of
     // the list the loads read zeros and the stores fill the unused stage.
-    q_from_lds();
+    if (n_tiles <= 0) q_from_lds();
     if (n_tiles > 0) {
       Staged sg;
       load_tile(tile_at(0), sg);
+      q_from_lds();   // overlaps the first tile's round trip
       store_tile(stage(0), sg);
       load_tile(tile_or_none(1), sg);
       __syncthreads();
