@@ -699,9 +699,19 @@ prefill_kernel(PrefillArgs a) {
     if (n_tiles > 0) {
       Staged sg;
       load_tile(tile_at(0), sg);
-      q_from_lds();   // overlaps the first tile's round trip
-      store_tile(stage(0), sg);
-      load_tile(tile_or_none(1), sg);
+      if constexpr (HALF) {
+        // half-tile shapes (GQA 5-8): tile 1 joins the same round trip
+        // (measured faster there, slower for the 2-wave GQA 1 shape)
+        Staged sg1;
+        load_tile(tile_or_none(1), sg1);
+        q_from_lds();
+        store_tile(stage(0), sg);
+        sg = sg1;
+      } else {
+        q_from_lds();   // overlaps the first tile's round trip
+        store_tile(stage(0), sg);
+        load_tile(tile_or_none(1), sg);
+      }
       __syncthreads();
       int kt_cur = tile_at(0);
       for (int it = 0; it < n_tiles; ++it) {
