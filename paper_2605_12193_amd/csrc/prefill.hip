@@ -132,6 +132,78 @@ __device__ __forceinline__ int uniform_load(const int32_t* p, int i) {
   return ((const_i32_ptr)p)[i];
 }
 
+// A block-table entry at byte offset e of a row, read as a scalar.  Through
+// readfirstlane: a plain load that feeds a select is sunk into a branch of
+// its own, and loads between branches are not issued together, which costs
+// one round trip per entry.
+__device__ __forceinline__ uint32_t table_entry(const int32_t* row, uint32_t e) {
+  typedef const __attribute__((address_space(4))) char* const_byte_ptr;
+  return (uint32_t)__builtin_amdgcn_readfirstlane(*(const_i32_ptr)((const_byte_ptr)row + e));
+}
+
+// Paged K/V: a 64-key tile spans up to four pages (pages hold >= 16 tokens).
+// Its keys are addressed as if the tile were contiguous, boff = (kr * st +
+// 8 ce) * 2 for key kr, plus the base of the key's page slot j = kr / ps
+// (0 when ps >= 64): base_j = pg_j * page_bytes + (tok0 % ps) * st * 2 -
+// j * ps * st * 2.  An entry outside [0, n_pages) gives 2^31, past every
+// descriptor's range, so its keys read zeros; rows counts the keys of the
+// tile below N_kv, and V units past it are zeroed the same way.  (Named
+// fields, not an array: per-lane picks among them must stay selects between
+// registers, not indexed scratch loads.)
+struct PageBases {
+  uint32_t b0, b1, b2, b3;
+  int rows;
+};
+// Tile kt of a request whose block-table row is bt (N_kv >= 1).  Tiles
+// outside [0, T_kv) (malformed lists) get rows = 0 and in-range bases: their
+// keys are masked and their values zeroed.  The four entries from the
+// tile's first page on are read unconditionally, clamped to the request's
+// last page, and issued together; slots past the tile or past N_kv are
+// never used for keys below N_kv.
+__device__ __forceinline__ PageBases page_bases(const int32_t* bt, int kt, int t_kv, int n_kv,
+                                                int ps_shift, uint32_t n_pages,
+                                                uint32_t page_bytes, uint32_t tok_bytes) {
+  const bool ok = (unsigned)kt < (unsigned)t_kv;
+  const int tok0 = ok ? kt * TILE : 0;
+  PageBases pb;
+  pb.rows = ok ? min(n_kv - tok0, TILE) : 0;
+  const uint32_t in_page = (uint32_t)(tok0 & ((1 << ps_shift) - 1)) * tok_bytes;
+  const uint32_t slot_step = tok_bytes << ps_shift;
+  const uint32_t e0 = (uint32_t)(tok0 >> ps_shift) * 4u;
+  const uint32_t last_e = (uint32_t)((n_kv - 1) >> ps_shift) * 4u;
+  uint32_t pg[4], b[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) pg[j] = table_entry(bt, min(e0 + 4u * j, last_e));
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    b[j] = pg[j] < n_pages ? pg[j] * page_bytes + in_page - (uint32_t)j * slot_step : 0x80000000u;
+  pb.b0 = b[0];
+  pb.b1 = b[1];
+  pb.b2 = b[2];
+  pb.b3 = b[3];
+  return pb;
+}
+// The four bases in lanes 0-3 of one register, written whatever the exec
+// mask (the other lanes are unused): a wave whose K rows of a round lie in
+// one page reads its base with one readlane.
+__device__ __forceinline__ int page_lanes(const PageBases pb) {
+  int vb;
+  asm("v_writelane_b32 %0, %1, 0" : "=v"(vb) : "s"(pb.b0));
+  asm("v_writelane_b32 %0, %1, 1" : "+v"(vb) : "s"(pb.b1));
+  asm("v_writelane_b32 %0, %1, 2" : "+v"(vb) : "s"(pb.b2));
+  asm("v_writelane_b32 %0, %1, 3" : "+v"(vb) : "s"(pb.b3));
+  return vb;
+}
+// V: a thread's key pair (2 j, 2 j + 1) lies in one page slot (hi, lo bits
+// of the slot index, fixed per thread); the base of each key, or 2^31 for a
+// key past N_kv.
+__device__ __forceinline__ void v_pair_bases(const PageBases pb, bool hi, bool lo, int key0,
+                                             uint32_t& b_first, uint32_t& b_second) {
+  const uint32_t bv = hi ? (lo ? pb.b3 : pb.b2) : (lo ? pb.b1 : pb.b0);
+  b_first = key0 < pb.rows ? bv : 0x80000000u;
+  b_second = key0 + 1 < pb.rows ? bv : 0x80000000u;
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
                                            (int)RSRC_WORD3);
@@ -324,6 +396,17 @@ prefill_kernel(PrefillArgs a) {
   }
   const uint32_t tile_bytes = (uint32_t)(TILE * st * 2);
   const uint32_t st_bytes = (uint32_t)(st * 2);
+  // page slot (0-3) inside a tile of this wave's K rows in round i, and of
+  // this thread's V key pair (paged K/V)
+  int kj[KC_PER_T];
+  {
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+    for (int i = 0; i < KC_PER_T; ++i)
+      kj[i] = ps < TILE ? ((wave_u * 64 + i * NT) / (C / 8)) >> ps_shift : 0;
+  }
+  const int v_slot = ps < TILE ? (2 * v_j[0]) >> ps_shift : 0;
+  const bool vj_hi = (v_slot & 2) != 0, vj_lo = (v_slot & 1) != 0;
 
   // one K/V tile on its way from memory to LDS, in registers
   struct Staged {
@@ -331,48 +414,14 @@ prefill_kernel(PrefillArgs a) {
     uint4 v[VU_PER_T][2];
   };
 
-  // Paged offsets from the chunk's offset inside a contiguous tile, boff =
-  // (kr * st + 8 ce) * 2 for key kr of the tile: the page slot of the chunk
-  // is the number of thresholds j * ps * st * 2 that boff reaches, and its
-  // byte offset is boff + base[slot], with base[j] = pg[j] * page_bytes +
-  // (tok0 % ps) * st * 2 - j * ps * st * 2 read per tile as scalars.  Keys
-  // past N_kv (boff >= (N_kv - tok0) * st * 2, as 8 ce + 8 <= C <= st) and bad
-  // pages give offsets >= 2^31, past the pool's range.
-  struct PagedTile {
-    uint32_t base[4];
-    uint32_t lim;
-  };
-  const uint32_t slot_bytes = ps < TILE ? (uint32_t)(ps * st * 2) : 0xFFFFFFFFu;
-  const uint32_t thr2 = ps < TILE / 2 ? 2 * slot_bytes : 0xFFFFFFFFu;
-  const uint32_t thr3 = ps < TILE / 2 ? 3 * slot_bytes : 0xFFFFFFFFu;
-  auto paged_off = [&](const PagedTile& pt, uint32_t boff) INLINE -> uint32_t {
-    if (boff >= pt.lim) return 0x80000000u;
-    const uint32_t b = boff < slot_bytes ? pt.base[0] : boff < thr2 ? pt.base[1]
-                     : boff < thr3 ? pt.base[2] : pt.base[3];
-    return b + boff;
-  };
-
-  // the page bases of tile kt (paged; read as scalars)
-  auto paged_tile = [&](int kt) INLINE -> PagedTile {
-    const bool ok = (unsigned)kt < (unsigned)t_kv;
-    const int tok0 = ok ? kt * TILE : 0;
-    PagedTile pt;
-    pt.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
-    const uint32_t in_page = (uint32_t)((tok0 & (ps - 1)) * st * 2);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tk = tok0 + (j << ps_shift);
-      const bool slot_used = j == 0 || (j << ps_shift) < TILE;  // pages this tile spans
-      const int pg = (ok && slot_used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
-      pt.base[j] = (unsigned)pg < (unsigned)a.kv.n_pages
-                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)(ps * st * 2)
-                       : 0x80000000u;
-    }
-    return pt;
+  // the page bases of tile kt (paged; scalars)
+  const uint32_t n_pages_u = (uint32_t)a.kv.n_pages;
+  auto paged_tile = [&](int kt) INLINE -> PageBases {
+    return page_bases(bt, kt, t_kv, n_kv, ps_shift, n_pages_u, page_bytes, st_bytes);
   };
   // Fetch this thread's K chunks (part & 1) and/or V units (part & 2) of
   // tile kt into sg.
-  auto load_part_pt = [&](int kt, const PagedTile& pt, Staged& sg, auto part) INLINE {
+  auto load_part_pt = [&](int kt, const PageBases pt, Staged& sg, auto part) INLINE {
     constexpr bool LK = (decltype(part)::value & 1) != 0, LV = (decltype(part)::value & 2) != 0;
     // tiles outside [0, T_kv) (malformed lists) load nothing
     const bool ok = (unsigned)kt < (unsigned)t_kv;
@@ -391,20 +440,33 @@ prefill_kernel(PrefillArgs a) {
         }
       return;
     }
+    // K: the keys one wave fetches in a round are 512 / C consecutive rows
+    // of the tile, inside one page, so the wave reads the base of that page
+    // (slot kj[i], fixed per wave) from page_lanes().  Keys past N_kv need no
+    // zeros: their scores are masked before the softmax.  V: a thread's key
+    // pair is the same in every round, so its bases are picked once per
+    // tile; values past N_kv read as zeros.
+    if constexpr (LK) {
+      const int vb = page_lanes(pt);
 #pragma unroll
-    for (int i = 0; i < KC_PER_T; ++i)
-      if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
-        sg.k[i] = bload16(krs, paged_off(pt, k_boff[i]));
+      for (int i = 0; i < KC_PER_T; ++i)
+        if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
+          sg.k[i] = bload16(krs, (uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + k_boff[i]);
+    }
+    if constexpr (LV) {
+      uint32_t b0, b1;
+      v_pair_bases(pt, vj_hi, vj_lo, 2 * v_j[0], b0, b1);
 #pragma unroll
-    for (int i = 0; i < VU_PER_T; ++i)
-      if (LV && (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS)) {
-        sg.v[i][0] = bload16(vrs, paged_off(pt, v_boff[i]));
-        sg.v[i][1] = bload16(vrs, paged_off(pt, v_boff[i] + st_bytes));
-      }
+      for (int i = 0; i < VU_PER_T; ++i)
+        if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
+          sg.v[i][0] = bload16(vrs, b0 + v_boff[i]);
+          sg.v[i][1] = bload16(vrs, b1 + v_boff[i] + st_bytes);
+        }
+    }
   };
   auto load_part = [&](int kt, Staged& sg, auto part) INLINE {
     if constexpr (PAGED) load_part_pt(kt, paged_tile(kt), sg, part);
-    else load_part_pt(kt, PagedTile{}, sg, part);
+    else load_part_pt(kt, PageBases{}, sg, part);
   };
   const std::integral_constant<int, 1> K_PART;
   const std::integral_constant<int, 2> V_PART;
@@ -618,7 +680,7 @@ prefill_kernel(PrefillArgs a) {
       load_tile(kt[2], sg0);
       load_tile(kt[3], sg1);
       // the page bases of tile i + 4, read outside the MFMA streams
-      PagedTile pt4{};
+      PageBases pt4{};
       if constexpr (PAGED) pt4 = paged_tile(kt[4]);
       __syncthreads();
       // Each group runs its own copy of the loop (same barriers in the same
@@ -775,54 +837,22 @@ prefill_kernel(PrefillArgs a) {
   }
 }
 
-// Where the keys of KV tile kt are, for the 16-query kernels, given a chunk's
-// byte offset inside a contiguous tile, boff = (kr * st + 8 ce) * 2 for key
-// kr of the tile.  Contiguous: the tile's first byte plus boff.  Paged, as in
-// prefill_kernel: per tile, scalar bases pg[j] * page_bytes + (tok0 % ps) *
-// st * 2 - j * ps * st * 2 of its (up to four) pages, a chunk taking the base
-// of the slot whose threshold j * ps * st * 2 its boff reaches.  Tiles
-// outside [0, T_kv), keys past N_kv and table entries outside the pool give
-// offsets past the descriptor's range, which read zeros.
-struct TileAt {
-  uint32_t base[4];
-  uint32_t lim;   // paged: boff of the first key past N_kv (or past the tile)
-};
 template <bool PAGED>
 struct KvTiles {
   int t_kv, n_kv;
   uint32_t tile_bytes;     // contiguous: bytes per 64-key tile
   const int32_t* bt;       // paged: this request's block-table row
-  int ps_shift, n_pages;
-  uint32_t page_bytes, slot_bytes, thr2, thr3;
+  int ps_shift;
+  uint32_t n_pages, page_bytes, tok_bytes;
   int64_t st;              // elements per token
 
-  __device__ __forceinline__ TileAt locate(int kt) const {
-    TileAt at;
-    const bool ok = (unsigned)kt < (unsigned)t_kv;
-    if (!PAGED) {
-      at.base[0] = ok ? (uint32_t)kt * tile_bytes : 0x80000000u;
-      return at;
-    }
-    const int tok0 = ok ? kt * TILE : 0;
-    at.lim = ok ? (uint32_t)(min(n_kv - tok0, TILE) * st * 2) : 0u;
-    const uint32_t in_page = (uint32_t)((tok0 & ((1 << ps_shift) - 1)) * st * 2);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tk = tok0 + (j << ps_shift);
-      const bool used = j == 0 || (j << ps_shift) < TILE;
-      const int pg = (ok && used && tk < n_kv) ? uniform_load(bt, tk >> ps_shift) : -1;
-      at.base[j] = (unsigned)pg < (unsigned)n_pages
-                       ? (uint32_t)pg * page_bytes + in_page - (uint32_t)j * (uint32_t)((st * 2) << ps_shift)
-                       : 0x80000000u;
-    }
-    return at;
-  }
-  __device__ __forceinline__ uint32_t off(const TileAt& at, uint32_t boff) const {
-    if (!PAGED) return at.base[0] + boff;
-    if (boff >= at.lim) return 0x80000000u;
-    const uint32_t b = boff < slot_bytes ? at.base[0] : boff < thr2 ? at.base[1]
-                     : boff < thr3 ? at.base[2] : at.base[3];
-    return b + boff;
+  // Contiguous: b0 is the tile's first byte (2^31 for a tile outside
+  // [0, T_kv), so its loads read zeros).  Paged: page_bases().
+  __device__ __forceinline__ PageBases locate(int kt) const {
+    if (PAGED) return page_bases(bt, kt, t_kv, n_kv, ps_shift, n_pages, page_bytes, tok_bytes);
+    PageBases pb{};
+    pb.b0 = (unsigned)kt < (unsigned)t_kv ? (uint32_t)kt * tile_bytes : 0x80000000u;
+    return pb;
   }
 };
 template <int C, bool PAGED>
@@ -841,20 +871,16 @@ __device__ __forceinline__ KvTiles<PAGED> kv_tiles(const PrefillArgs& a, const R
     vrs = make_rsrc(a.kv.v + head_off, bytes);
     kt.bt = nullptr;
     kt.ps_shift = 0;
-    kt.n_pages = 0;
-    kt.page_bytes = kt.slot_bytes = kt.thr2 = kt.thr3 = 0;
+    kt.n_pages = kt.page_bytes = kt.tok_bytes = 0;
   } else {
     const int64_t head_off = (int64_t)h * a.kv.stride_head;
     krs = make_rsrc(a.kv.k + head_off, a.kv.pool_bytes);
     vrs = make_rsrc(a.kv.v + head_off, a.kv.pool_bytes);
     kt.bt = a.kv.block_table + (int64_t)Rd.bt_row * a.kv.max_pages;
     kt.ps_shift = __builtin_ctz(a.kv.page_size);   // power of two >= 16
-    kt.n_pages = a.kv.n_pages;
+    kt.n_pages = (uint32_t)a.kv.n_pages;
     kt.page_bytes = (uint32_t)(a.kv.page_stride * 2);
-    const int ps = a.kv.page_size;
-    kt.slot_bytes = ps < TILE ? (uint32_t)(ps * kt.st * 2) : 0xFFFFFFFFu;
-    kt.thr2 = ps < TILE / 2 ? 2 * kt.slot_bytes : 0xFFFFFFFFu;
-    kt.thr3 = ps < TILE / 2 ? 3 * kt.slot_bytes : 0xFFFFFFFFu;
+    kt.tok_bytes = (uint32_t)(kt.st * 2);
   }
   return kt;
 }
@@ -985,18 +1011,42 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   const uint32_t st_bytes = (uint32_t)(st * 2);
   struct KSet { uint4 k[KC_PER_T]; };
   struct VSet { uint4 v[VU_PER_T][2]; };
-  auto locate = [&](int kt) INLINE -> TileAt { return kvt.locate(kt); };
-  auto load_k_at = [&](const TileAt& at, KSet& sk) INLINE {
+  // Paged: the page slot (0-3) of this wave's K rows in round i (two
+  // consecutive rows, inside one page) and of this thread's V key pair.
+  int kj[KC_PER_T];
+  bool vj_hi = false, vj_lo = false;
+  if constexpr (PAGED) {
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const bool paged_slots = kvt.ps_shift < 6;   // pages shorter than a tile
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
-      if (k_mine(i)) sk.k[i] = bload16(krs, kvt.off(at, k_boff[i]));
+      kj[i] = paged_slots ? ((wave_u * 64 + i * NT) / (C / 8)) >> kvt.ps_shift : 0;
+    const int v_slot = paged_slots ? (2 * v_j[0]) >> kvt.ps_shift : 0;
+    vj_hi = (v_slot & 2) != 0;
+    vj_lo = (v_slot & 1) != 0;
+  }
+  auto locate = [&](int kt) INLINE -> PageBases { return kvt.locate(kt); };
+  auto load_k_at = [&](const PageBases at, KSet& sk) INLINE {
+    if constexpr (PAGED) {
+      const int vb = page_lanes(at);
+#pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i)
+        if (k_mine(i))
+          sk.k[i] = bload16(krs, (uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + k_boff[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < KC_PER_T; ++i)
+        if (k_mine(i)) sk.k[i] = bload16(krs, at.b0 + k_boff[i]);
+    }
   };
-  auto load_v_at = [&](const TileAt& at, VSet& sv) INLINE {
+  auto load_v_at = [&](const PageBases at, VSet& sv) INLINE {
+    uint32_t b0 = at.b0, b1 = at.b0;
+    if constexpr (PAGED) v_pair_bases(at, vj_hi, vj_lo, 2 * v_j[0], b0, b1);
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (v_mine(i)) {
-        sv.v[i][0] = bload16(vrs, kvt.off(at, v_boff[i]));
-        sv.v[i][1] = bload16(vrs, kvt.off(at, v_boff[i] + st_bytes));
+        sv.v[i][0] = bload16(vrs, b0 + v_boff[i]);
+        sv.v[i][1] = bload16(vrs, b1 + v_boff[i] + st_bytes);
       }
   };
   auto load_k = [&](int kt, KSet& sk) INLINE { load_k_at(kvt.locate(kt), sk); };
@@ -1158,7 +1208,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       load_v(kt[1], sv);
       // where the next fetches go, K of tile i + 3 and V of tile i + 2, read
       // at the end of the previous iteration (paged: outside the MFMA streams)
-      TileAt at_k = locate(kt[3]), at_v = locate(kt[2]);
+      PageBases at_k = locate(kt[3]), at_v = locate(kt[2]);
       __syncthreads();
       auto run = [&](auto is_a) INLINE {
         constexpr bool A = decltype(is_a)::value;
@@ -1228,7 +1278,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       int kt[2];
       kt[0] = tile_or_none(0);
       kt[1] = tile_or_none(1);
-      TileAt at1 = locate(kt[0]);
+      PageBases at1 = locate(kt[0]);
       load_k_at(at1, sk);
   #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
@@ -1290,13 +1340,13 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       int kt[3];
   #pragma unroll
       for (int j = 0; j < 3; ++j) kt[j] = tile_or_none(j);
-      TileAt at1 = locate(kt[0]);
+      PageBases at1 = locate(kt[0]);
       load_k_at(at1, sk);
   #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i) store_k(0, sk, i);
       load_v_at(at1, sv);
       at1 = locate(kt[1]);
-      TileAt at2 = locate(kt[2]);
+      PageBases at2 = locate(kt[2]);
       load_k_at(at1, sk);
       __syncthreads();
       constexpr int L0 = 2 + 2 * (KC_PER_T + VU_PER_T);

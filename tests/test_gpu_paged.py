@@ -119,3 +119,64 @@ def test_paged_stage1_with_wide_groups():
                          O.default_scale(c))
     mask_compare(got[0][0][:st["mask"].size].reshape(st["mask"].shape), st["mask"],
                  st["status"])
+
+
+def test_out_of_range_table_entries_read_as_zeros():
+    # A block-table entry outside [0, n_pages) reads as zeros in every kernel:
+    # the paged run with such entries equals, bit for bit, the contiguous run
+    # whose K/V rows of those pages are zero (Stage 1 scores and masks, tile
+    # lists, sparse and dense outputs, LSE), and the sparse output matches
+    # the oracle on the zeroed inputs.  Bad pages sit in the first, a middle
+    # and the last (partial) tile, and one spans a whole 64-key tile.
+    seqlens, n_q, h_q, h_kv, c = [700, 333], [700, 333], 10, 2, 128
+    wl = synth.workload("paged_4x", seqlens=seqlens, h_q=h_q, h_kv=h_kv, head_dim=c)
+    seqs = synth.make_inputs(wl)
+    pb = PagedBatch(seqs, n_q, 16, wl.seed)
+    n_pages = int(pb.kp.shape[0])
+    bad = {0: {0: -1, 17: n_pages, 20: n_pages + 5, 21: -7, 22: 2 ** 30, 23: -(2 ** 31), 43: n_pages},
+           1: {5: -1, 20: n_pages + 1}}
+    table = pb.table.cpu().numpy()
+    zeroed = []
+    for r, s in enumerate(seqs):
+        k, v = s.k.clone(), s.v.clone()
+        for page, val in bad[r].items():
+            assert page * 16 < seqlens[r]
+            table[r, page] = val
+            k[:, page * 16:(page + 1) * 16] = 0
+            v[:, page * 16:(page + 1) * 16] = 0
+        zeroed.append(synth.Sequence(q=s.q, k=k, v=v))
+    pb.table.copy_(torch.from_numpy(table))
+    db = DeviceBatch(zeroed, n_q)
+    prm = bfla.params(block=wl.block, group=wl.group, tile=wl.tile, gamma=wl.gamma,
+                      n_local=wl.n_local, n_sink=wl.n_sink, eta=wl.eta, rho=wl.rho,
+                      seed=wl.seed)
+    outs = []
+    for b in (pb, db):
+        buf = bfla.Buffers(b.prob, prm)
+        bfla.bfla_estimate_mask(b.prob, prm, b.qv, b.kv, buf.block_mask, dbg_scores=buf.scores,
+                                workspace=buf.ws_estimate)
+        bfla.bfla_expand_rescue(b.prob, prm, buf.block_mask, buf.row_ptr, buf.cols,
+                                buf.ws_expand)
+        bfla.bfla_sparse_prefill(b.prob, prm, b.qv, b.kv, buf.row_ptr, buf.cols, b.ov, buf.lse)
+        torch.cuda.synchronize()
+        rp = buf.row_ptr.cpu().numpy()
+        sparse = [b.o_of(r) for r in range(len(seqs))]
+        bfla.bfla_dense_prefill(b.prob, prm, b.qv, b.kv, b.ov)
+        torch.cuda.synchronize()
+        outs.append(dict(mask=buf.block_mask.cpu().numpy(), scores=buf.scores.cpu().numpy(),
+                         rp=rp, cols=buf.cols[:int(rp[-1])].cpu().numpy(),
+                         lse=buf.lse.cpu().numpy(), sparse=sparse,
+                         dense=[b.o_of(r) for r in range(len(seqs))]))
+    p, d = outs
+    for key in ("mask", "scores", "rp", "cols", "lse"):
+        assert np.array_equal(p[key], d[key], equal_nan=True), key
+    for r in range(len(seqs)):
+        assert np.array_equal(p["sparse"][r], d["sparse"][r]), f"sparse request {r}"
+        assert np.array_equal(p["dense"][r], d["dense"][r]), f"dense request {r}"
+    alpha = O.default_scale(c)
+    base = 0
+    for r, s in enumerate(zeroed):
+        want, _ = O.attention(s.q.double().numpy(), s.k.double().numpy(), s.v.double().numpy(),
+                              wl.tile, alpha, p["rp"], p["cols"], base)
+        base += h_kv * -(-n_q[r] // wl.tile)
+        compare_outputs(p["sparse"][r], want, f"request {r} with bad pages")
