@@ -155,11 +155,11 @@ struct PageBases {
   int rows;
 };
 // Tile kt of a request whose block-table row is bt (N_kv >= 1).  Tiles
-// outside [0, T_kv) (malformed lists) get rows = 0 and in-range bases: their
-// keys are masked and their values zeroed.  The four entries from the
-// tile's first page on are read unconditionally, clamped to the request's
-// last page, and issued together; slots past the tile or past N_kv are
-// never used for keys below N_kv.
+// outside [0, T_kv) (past the end of a list, or malformed lists) get rows = 0
+// and bases of 2^31: their loads read zeros without memory traffic.  The
+// four entries from the tile's first page on are read unconditionally,
+// clamped to the request's last page, and issued together; slots past the
+// tile or past N_kv are never used for keys below N_kv.
 __device__ __forceinline__ PageBases page_bases(const int32_t* bt, int kt, int t_kv, int n_kv,
                                                 int ps_shift, uint32_t n_pages,
                                                 uint32_t page_bytes, uint32_t tok_bytes) {
@@ -176,7 +176,8 @@ __device__ __forceinline__ PageBases page_bases(const int32_t* bt, int kt, int t
   for (int j = 0; j < 4; ++j) pg[j] = table_entry(bt, min(e0 + 4u * j, last_e));
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    b[j] = pg[j] < n_pages ? pg[j] * page_bytes + in_page - (uint32_t)j * slot_step : 0x80000000u;
+    b[j] = ok && pg[j] < n_pages ? pg[j] * page_bytes + in_page - (uint32_t)j * slot_step
+                                 : 0x80000000u;
   pb.b0 = b[0];
   pb.b1 = b[1];
   pb.b2 = b[2];
@@ -373,27 +374,23 @@ prefill_kernel(PrefillArgs a) {
   const int ps_shift = __builtin_ctz(ps);
   const uint32_t page_bytes = (uint32_t)(a.kv.page_stride * 2);
   const int32_t* bt = a.kv.block_table + (int64_t)bt_row * a.kv.max_pages;
-  // per-thread constant parts of the staging pattern
-  int k_row[KC_PER_T], k_ce[KC_PER_T];
-  uint32_t k_boff[KC_PER_T];  // byte offset inside a contiguous tile
-#pragma unroll
-  for (int i = 0; i < KC_PER_T; ++i) {
-    int e = tid + i * NT;
-    k_row[i] = e / (C / 8);
-    k_ce[i] = e % (C / 8);
-    k_boff[i] = (uint32_t)(((int64_t)k_row[i] * st + 8 * k_ce[i]) * 2);
-  }
-  int v_j[VU_PER_T], v_ce[VU_PER_T];
-  uint32_t v_boff[VU_PER_T];
-#pragma unroll
-  for (int i = 0; i < VU_PER_T; ++i) {
-    // key pair fastest: the 16 lanes of one LDS store phase write 16
-    // consecutive words of one V^T row (distinct banks)
-    int u = tid + i * NT;
-    v_j[i] = u % (TILE / 2);
-    v_ce[i] = u / (TILE / 2);
-    v_boff[i] = (uint32_t)(((int64_t)(2 * v_j[i]) * st + 8 * v_ce[i]) * 2);
-  }
+  // Per-thread constant parts of the staging pattern.  A thread stages K
+  // chunks e = tid + i NT (row e / (C / 8), channels 8 (e % (C / 8)) on) and
+  // V units u = tid + i NT (key pair u % 32, fastest, so that the 16 lanes of
+  // one LDS store phase write 16 consecutive words of one V^T row; channels
+  // 8 (u / 32) on).  NT is a multiple of C / 8 and of 32, so round i only
+  // moves the K row by i K_ROW_STEP and the V channel group by i V_CE_STEP:
+  // one register holds each offset of round 0 and the steps are scalars or
+  // immediates (offsets kept per round would hold KC_PER_T + VU_PER_T VGPRs
+  // for the whole kernel).
+  constexpr int K_ROW_STEP = NT / (C / 8), V_CE_STEP = NT / (TILE / 2);
+  static_assert(NT % (C / 8) == 0 && NT % (TILE / 2) == 0, "rounds must keep a thread's column");
+  const int k_row = tid / (C / 8), k_ce = tid % (C / 8);
+  const uint32_t k_boff = (uint32_t)(((int64_t)k_row * st + 8 * k_ce) * 2);  // round 0, in a tile
+  const uint32_t k_step = (uint32_t)(K_ROW_STEP * st * 2);
+  const int v_j = tid % (TILE / 2), v_ce = tid / (TILE / 2);
+  const uint32_t v_boff = (uint32_t)(((int64_t)(2 * v_j) * st + 8 * v_ce) * 2);
+  constexpr uint32_t V_STEP = V_CE_STEP * 8 * 2;
   const uint32_t tile_bytes = (uint32_t)(TILE * st * 2);
   const uint32_t st_bytes = (uint32_t)(st * 2);
   // page slot (0-3) inside a tile of this wave's K rows in round i, and of
@@ -405,7 +402,7 @@ prefill_kernel(PrefillArgs a) {
     for (int i = 0; i < KC_PER_T; ++i)
       kj[i] = ps < TILE ? ((wave_u * 64 + i * NT) / (C / 8)) >> ps_shift : 0;
   }
-  const int v_slot = ps < TILE ? (2 * v_j[0]) >> ps_shift : 0;
+  const int v_slot = ps < TILE ? (2 * v_j) >> ps_shift : 0;
   const bool vj_hi = (v_slot & 2) != 0, vj_lo = (v_slot & 1) != 0;
 
   // one K/V tile on its way from memory to LDS, in registers
@@ -431,12 +428,12 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
         if (LK && (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS))
-          sg.k[i] = bload16(krs, base + k_boff[i]);
+          sg.k[i] = bload16(krs, (base + i * k_step) + k_boff);
 #pragma unroll
       for (int i = 0; i < VU_PER_T; ++i)
         if (LV && (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS)) {
-          sg.v[i][0] = bload16(vrs, base + v_boff[i]);
-          sg.v[i][1] = bload16(vrs, base + v_boff[i] + st_bytes);
+          sg.v[i][0] = bload16(vrs, base + v_boff + i * V_STEP);
+          sg.v[i][1] = bload16(vrs, (base + st_bytes) + v_boff + i * V_STEP);
         }
       return;
     }
@@ -451,16 +448,18 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
         if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-          sg.k[i] = bload16(krs, (uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + k_boff[i]);
+          sg.k[i] = bload16(krs, ((uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + i * k_step) + k_boff);
     }
     if constexpr (LV) {
       uint32_t b0, b1;
-      v_pair_bases(pt, vj_hi, vj_lo, 2 * v_j[0], b0, b1);
+      v_pair_bases(pt, vj_hi, vj_lo, 2 * v_j, b0, b1);
+      b0 += v_boff;
+      b1 += v_boff + st_bytes;
 #pragma unroll
       for (int i = 0; i < VU_PER_T; ++i)
         if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-          sg.v[i][0] = bload16(vrs, b0 + v_boff[i]);
-          sg.v[i][1] = bload16(vrs, b1 + v_boff[i] + st_bytes);
+          sg.v[i][0] = bload16(vrs, b0 + i * V_STEP);
+          sg.v[i][1] = bload16(vrs, b1 + i * V_STEP);
         }
     }
   };
@@ -477,14 +476,14 @@ prefill_kernel(PrefillArgs a) {
   // K chunk i, and V unit i (two keys x 8 channels, transposed on the way).
   auto store_k = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
     if (CF::K_CHUNKS % NT == 0 || tid + i * NT < CF::K_CHUNKS)
-      *reinterpret_cast<uint4*>(stg + k_row[i] * CF::KROW + 8 * k_ce[i]) = sg.k[i];
+      *reinterpret_cast<uint4*>(stg + k_row * CF::KROW + 8 * k_ce + i * K_ROW_STEP * CF::KROW) = sg.k[i];
   };
   auto store_v = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
     if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-      const int pos = vperm(2 * v_j[i]);
+      const int pos = vperm(2 * v_j);
       const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
       const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
-      bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce[i] * CF::VROW + pos;
+      bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce * CF::VROW + pos + i * 8 * V_CE_STEP * CF::VROW;
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
         // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
@@ -988,24 +987,16 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   __amdgpu_buffer_rsrc_t krs, vrs;
   const KvTiles<PAGED> kvt = kv_tiles<C, PAGED>(a, Rd, h, krs, vrs);
   const int64_t st = a.kv.stride_tok;
-  int k_row[KC_PER_T], k_ce[KC_PER_T];
-  uint32_t k_boff[KC_PER_T];
-#pragma unroll
-  for (int i = 0; i < KC_PER_T; ++i) {
-    const int e = tid + i * NT;
-    k_row[i] = e / (C / 8);
-    k_ce[i] = e % (C / 8);
-    k_boff[i] = (uint32_t)(((int64_t)k_row[i] * st + 8 * k_ce[i]) * 2);
-  }
-  int v_j[VU_PER_T], v_ce[VU_PER_T];
-  uint32_t v_boff[VU_PER_T];
-#pragma unroll
-  for (int i = 0; i < VU_PER_T; ++i) {
-    const int u = tid + i * NT;
-    v_j[i] = u % (TILE / 2);
-    v_ce[i] = u / (TILE / 2);
-    v_boff[i] = (uint32_t)(((int64_t)(2 * v_j[i]) * st + 8 * v_ce[i]) * 2);
-  }
+  // staging pattern as in prefill_kernel: round i moves a thread's K row by
+  // i K_ROW_STEP and its V channel group by i V_CE_STEP
+  constexpr int K_ROW_STEP = NT / (C / 8), V_CE_STEP = NT / (TILE / 2);
+  static_assert(NT % (C / 8) == 0 && NT % (TILE / 2) == 0, "rounds must keep a thread's column");
+  const int k_row = tid / (C / 8), k_ce = tid % (C / 8);
+  const uint32_t k_boff = (uint32_t)(((int64_t)k_row * st + 8 * k_ce) * 2);
+  const uint32_t k_step = (uint32_t)(K_ROW_STEP * st * 2);
+  const int v_j = tid % (TILE / 2), v_ce = tid / (TILE / 2);
+  const uint32_t v_boff = (uint32_t)(((int64_t)(2 * v_j) * st + 8 * v_ce) * 2);
+  constexpr uint32_t V_STEP = V_CE_STEP * 8 * 2;
   auto k_mine = [&](int i) INLINE { return K_CHUNKS % NT == 0 || tid + i * NT < K_CHUNKS; };
   auto v_mine = [&](int i) INLINE { return V_UNITS % NT == 0 || tid + i * NT < V_UNITS; };
   const uint32_t st_bytes = (uint32_t)(st * 2);
@@ -1021,7 +1012,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
 #pragma unroll
     for (int i = 0; i < KC_PER_T; ++i)
       kj[i] = paged_slots ? ((wave_u * 64 + i * NT) / (C / 8)) >> kvt.ps_shift : 0;
-    const int v_slot = paged_slots ? (2 * v_j[0]) >> kvt.ps_shift : 0;
+    const int v_slot = paged_slots ? (2 * v_j) >> kvt.ps_shift : 0;
     vj_hi = (v_slot & 2) != 0;
     vj_lo = (v_slot & 1) != 0;
   }
@@ -1032,21 +1023,23 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
         if (k_mine(i))
-          sk.k[i] = bload16(krs, (uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + k_boff[i]);
+          sk.k[i] = bload16(krs, ((uint32_t)__builtin_amdgcn_readlane(vb, kj[i]) + i * k_step) + k_boff);
     } else {
 #pragma unroll
       for (int i = 0; i < KC_PER_T; ++i)
-        if (k_mine(i)) sk.k[i] = bload16(krs, at.b0 + k_boff[i]);
+        if (k_mine(i)) sk.k[i] = bload16(krs, (at.b0 + i * k_step) + k_boff);
     }
   };
   auto load_v_at = [&](const PageBases at, VSet& sv) INLINE {
     uint32_t b0 = at.b0, b1 = at.b0;
-    if constexpr (PAGED) v_pair_bases(at, vj_hi, vj_lo, 2 * v_j[0], b0, b1);
+    if constexpr (PAGED) v_pair_bases(at, vj_hi, vj_lo, 2 * v_j, b0, b1);
+    b0 += v_boff;
+    b1 += v_boff + st_bytes;
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i)
       if (v_mine(i)) {
-        sv.v[i][0] = bload16(vrs, b0 + v_boff[i]);
-        sv.v[i][1] = bload16(vrs, b1 + v_boff[i] + st_bytes);
+        sv.v[i][0] = bload16(vrs, b0 + i * V_STEP);
+        sv.v[i][1] = bload16(vrs, b1 + i * V_STEP);
       }
   };
   auto load_k = [&](int kt, KSet& sk) INLINE { load_k_at(kvt.locate(kt), sk); };
@@ -1055,14 +1048,14 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   bf16_t* const vring = lds + 2 * K_SLOT;     // [2][V_SLOT]
   auto store_k = [&](int slot, const KSet& sk, int i) INLINE {
     if (k_mine(i))
-      *reinterpret_cast<uint4*>(kring + slot * K_SLOT + k_row[i] * KROW + 8 * k_ce[i]) = sk.k[i];
+      *reinterpret_cast<uint4*>(kring + slot * K_SLOT + k_row * KROW + 8 * k_ce + i * K_ROW_STEP * KROW) = sk.k[i];
   };
   auto store_v = [&](int slot, const VSet& sv, int i) INLINE {
     if (!v_mine(i)) return;
-    const int pos = vperm16(2 * v_j[i]);
+    const int pos = vperm16(2 * v_j);
     const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sv.v[i][0]);
     const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sv.v[i][1]);
-    bf16_t* col = vring + slot * V_SLOT + 8 * v_ce[i] * VROW + pos;
+    bf16_t* col = vring + slot * V_SLOT + 8 * v_ce * VROW + pos + i * 8 * V_CE_STEP * VROW;
 #pragma unroll
     for (int e2 = 0; e2 < 4; ++e2) {
       const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
