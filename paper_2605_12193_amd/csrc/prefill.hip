@@ -338,8 +338,10 @@ prefill_kernel(PrefillArgs a) {
     const bf16_t* const qb = a.q + q_off + (int64_t)p * a.q_sh;
 #pragma unroll
     for (int i = 0; i < 32 / QRPI; ++i) {
-      const int r = r0 + QRPI * i;
-      qv[i] = t0 + r < n_q ? ld16(qb + (int64_t)(t0 + r) * a.q_st + ch) : make_uint4(0, 0, 0, 0);
+      // rows past N_q (never stored) repeat the last query: the loads need
+      // no branch, and the compiler then issues them back to back
+      const int r = min(t0 + r0 + QRPI * i, n_q - 1);
+      qv[i] = ld16(qb + (int64_t)r * a.q_st + ch);
     }
   }
   auto q_from_lds = [&]() INLINE {
@@ -522,8 +524,20 @@ prefill_kernel(PrefillArgs a) {
   // read itself is unconditional (index clamped) so that it stays a scalar
   // load: a vector load would share vmcnt with the K/V prefetch.
   auto tile_or_none = [&](int i) INLINE -> int {
-    const int t = tile_at(min(i, n_tiles - 1));
+    // (through readfirstlane: a plain load feeding the select would be sunk
+    // into a branch of its own)
+    const int t = __builtin_amdgcn_readfirstlane(tile_at(min(i, n_tiles - 1)));
     return i < n_tiles ? t : -1;
+  };
+  // entries first .. first + N - 1, all read before the first is used (one
+  // round trip instead of N)
+  auto tiles_or_none = [&](int first, auto& kt) INLINE {
+    constexpr int N = sizeof(kt) / sizeof(kt[0]);
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+      kt[j] = __builtin_amdgcn_readfirstlane(tile_at(min(first + j, n_tiles - 1)));
+#pragma unroll
+    for (int j = 0; j < N; ++j) kt[j] = first + j < n_tiles ? kt[j] : -1;
   };
 
   // ---- MFMA streams fed from LDS ----
@@ -669,8 +683,7 @@ prefill_kernel(PrefillArgs a) {
     if (n_tiles > 0) {
       Staged sg0, sg1;
       int kt[5];  // tiles i .. i+4
-#pragma unroll
-      for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
+      tiles_or_none(0, kt);
       load_tile(kt[0], sg0);
       load_tile(kt[1], sg1);
       q_from_lds();
@@ -759,22 +772,26 @@ prefill_kernel(PrefillArgs a) {
     if (n_tiles <= 0) q_from_lds();
     if (n_tiles > 0) {
       Staged sg;
-      load_tile(tile_at(0), sg);
+      int kt01[2];   // list entries 0 and 1
+      tiles_or_none(0, kt01);
+      load_tile(kt01[0], sg);
       if constexpr (HALF) {
         // half-tile shapes (GQA 5-8): tile 1 joins the same round trip
         // (measured faster there, slower for the 2-wave GQA 1 shape)
         Staged sg1;
-        load_tile(tile_or_none(1), sg1);
+        load_tile(kt01[1], sg1);
         q_from_lds();
         store_tile(stage(0), sg);
         sg = sg1;
       } else {
         q_from_lds();   // overlaps the first tile's round trip
         store_tile(stage(0), sg);
-        load_tile(tile_or_none(1), sg);
+        load_tile(kt01[1], sg);
       }
       __syncthreads();
-      int kt_cur = tile_at(0);
+      // tiles it and it + 1; each entry is read once, as the fetch of
+      // iteration it - 2 (entry it) and carried
+      int kt_cur = kt01[0], kt_next = kt01[1];
       for (int it = 0; it < n_tiles; ++it) {
         bf16_t* const dst = stage((it + 1) & 1);
         const int kt_load = tile_or_none(it + 2);
@@ -789,7 +806,8 @@ prefill_kernel(PrefillArgs a) {
         stream(NO, YES, 0, it & 1, no_hook);
         softmax(kt_cur);
         stream(YES, NO, it & 1, 0, stage_hook);
-        kt_cur = tile_or_none(it + 1);
+        kt_cur = kt_next;
+        kt_next = kt_load;
         __syncthreads();
       }
     }
@@ -977,10 +995,10 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
 
   bf16x8 qf[NKC];
   {
-    const bf16_t* qp = a.q + q_off + (int64_t)p * a.q_sh + (int64_t)t * a.q_st + 8 * g;
+    // queries past N_q (never stored) repeat the last one: no branch
+    const bf16_t* qp = a.q + q_off + (int64_t)p * a.q_sh + (int64_t)min(t, n_q - 1) * a.q_st + 8 * g;
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      qf[kc] = as_bf16x8(t < n_q ? ld16(qp + 32 * kc) : make_uint4(0, 0, 0, 0));
+    for (int kc = 0; kc < NKC; ++kc) qf[kc] = as_bf16x8(ld16(qp + 32 * kc));
   }
   __builtin_amdgcn_s_waitcnt(VMCNT0);
 
@@ -1066,8 +1084,19 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
   };
   auto tile_or_none = [&](int i) INLINE -> int {
     if (DENSE) return i < n_tiles ? i : -1;
-    const int tt = uniform_load(a.cols, __builtin_amdgcn_readfirstlane(list_begin + min(i, n_tiles - 1)));
+    const int tt = __builtin_amdgcn_readfirstlane(
+        uniform_load(a.cols, __builtin_amdgcn_readfirstlane(list_begin + min(i, n_tiles - 1))));
     return i < n_tiles ? tt : -1;
+  };
+  // entries 0 .. N - 1, all read before the first is used
+  auto first_tiles = [&](auto& kt) INLINE {
+    constexpr int N = sizeof(kt) / sizeof(kt[0]);
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+      kt[j] = DENSE ? j : __builtin_amdgcn_readfirstlane(uniform_load(
+                              a.cols, __builtin_amdgcn_readfirstlane(list_begin + min(j, n_tiles - 1))));
+#pragma unroll
+    for (int j = 0; j < N; ++j) kt[j] = j < n_tiles ? kt[j] : -1;
   };
 
   const float c2 = a.scale * LOG2E;
@@ -1186,8 +1215,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       KSet sk;
       VSet sv;
       int kt[5];   // tiles i .. i + 4
-  #pragma unroll
-      for (int j = 0; j < 5; ++j) kt[j] = tile_or_none(j);
+      first_tiles(kt);
       load_k(kt[0], sk);
       load_v(kt[0], sv);
   #pragma unroll
@@ -1269,8 +1297,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       KSet sk;
       VSet sv;
       int kt[2];
-      kt[0] = tile_or_none(0);
-      kt[1] = tile_or_none(1);
+      first_tiles(kt);
       PageBases at1 = locate(kt[0]);
       load_k_at(at1, sk);
   #pragma unroll
@@ -1331,8 +1358,7 @@ __global__ void __launch_bounds__(64 * M * q16_blocks(M)) prefill_q16_kernel(Pre
       KSet sk;
       VSet sv;
       int kt[3];
-  #pragma unroll
-      for (int j = 0; j < 3; ++j) kt[j] = tile_or_none(j);
+      first_tiles(kt);
       PageBases at1 = locate(kt[0]);
       load_k_at(at1, sk);
   #pragma unroll
