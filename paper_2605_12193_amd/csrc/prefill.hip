@@ -407,10 +407,33 @@ prefill_kernel(PrefillArgs a) {
   const int v_slot = ps < TILE ? (2 * v_j) >> ps_shift : 0;
   const bool vj_hi = (v_slot & 2) != 0, vj_lo = (v_slot & 1) != 0;
 
+  // Ping-pong shapes split the staging between the groups instead: group A
+  // (waves 0-3) stages every V unit of a tile, group B (waves 4-7) every K
+  // chunk, each with the pattern above over its GT threads.
+  constexpr int GT = NT / 2;
+  constexpr int KC_B = PP ? CF::K_CHUNKS / GT : 0, VU_A = PP ? CF::V_UNITS / GT : 0;
+  static_assert(!PP || (CF::K_CHUNKS % GT == 0 && CF::V_UNITS % GT == 0), "group staging");
+  constexpr int K_ROW_STEP_G = GT / (C / 8), V_CE_STEP_G = GT / (TILE / 2);
+  const int gtid = tid & (GT - 1);
+  const int k_row_g = gtid / (C / 8), k_ce_g = gtid % (C / 8);
+  const uint32_t k_boff_g = (uint32_t)(((int64_t)k_row_g * st + 8 * k_ce_g) * 2);
+  const uint32_t k_step_g = (uint32_t)(K_ROW_STEP_G * st * 2);
+  const int v_ce_g = gtid / (TILE / 2);   // v_j is the same as above
+  const uint32_t v_boff_g = (uint32_t)(((int64_t)(2 * v_j) * st + 8 * v_ce_g) * 2);
+  constexpr uint32_t V_STEP_G = V_CE_STEP_G * 8 * 2;
+  int kj_g[KC_B > 0 ? KC_B : 1];   // group B: page slot of the wave's K rows in round i
+  {
+    const int wave_g = __builtin_amdgcn_readfirstlane(wave) & 3;
+#pragma unroll
+    for (int i = 0; i < KC_B; ++i)
+      kj_g[i] = ps < TILE ? ((wave_g * 64 + i * GT) / (C / 8)) >> ps_shift : 0;
+  }
+
   // one K/V tile on its way from memory to LDS, in registers
+  constexpr int KS = KC_PER_T > KC_B ? KC_PER_T : KC_B, VS = VU_PER_T > VU_A ? VU_PER_T : VU_A;
   struct Staged {
-    uint4 k[KC_PER_T];
-    uint4 v[VU_PER_T][2];
+    uint4 k[KS];
+    uint4 v[VS][2];
   };
 
   // the page bases of tile kt (paged; scalars)
@@ -501,6 +524,51 @@ prefill_kernel(PrefillArgs a) {
     for (int i = 0; i < KC_PER_T; ++i) store_k(stg, sg, i);
 #pragma unroll
     for (int i = 0; i < VU_PER_T; ++i) store_v(stg, sg, i);
+  };
+  // ping-pong group staging: B fetches / stores K chunk i (i < KC_B), A V
+  // unit i (i < VU_A)
+  auto load_k_b = [&](int kt, const PageBases pt, Staged& sg) INLINE {
+    if constexpr (PAGED) {
+      const int vb = page_lanes(pt);
+#pragma unroll
+      for (int i = 0; i < KC_B; ++i)
+        sg.k[i] = bload16(krs, ((uint32_t)__builtin_amdgcn_readlane(vb, kj_g[i]) + i * k_step_g) + k_boff_g);
+    } else {
+      const uint32_t base = (unsigned)kt < (unsigned)t_kv ? (uint32_t)kt * tile_bytes : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < KC_B; ++i) sg.k[i] = bload16(krs, (base + i * k_step_g) + k_boff_g);
+    }
+  };
+  auto load_v_a = [&](int kt, const PageBases pt, Staged& sg) INLINE {
+    uint32_t b0, b1;
+    if constexpr (PAGED) {
+      v_pair_bases(pt, vj_hi, vj_lo, 2 * v_j, b0, b1);
+    } else {
+      b0 = b1 = (unsigned)kt < (unsigned)t_kv ? (uint32_t)kt * tile_bytes : 0x80000000u;
+    }
+    b0 += v_boff_g;
+    b1 += v_boff_g + st_bytes;
+#pragma unroll
+    for (int i = 0; i < VU_A; ++i) {
+      sg.v[i][0] = bload16(vrs, b0 + i * V_STEP_G);
+      sg.v[i][1] = bload16(vrs, b1 + i * V_STEP_G);
+    }
+  };
+  auto store_k_b = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    *reinterpret_cast<uint4*>(stg + k_row_g * CF::KROW + 8 * k_ce_g + i * K_ROW_STEP_G * CF::KROW) = sg.k[i];
+  };
+  auto store_v_a = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    const int pos = vperm(2 * v_j);
+    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
+    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
+    bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce_g * CF::VROW + pos + i * 8 * V_CE_STEP_G * CF::VROW;
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2) {
+      const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
+      const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
+      *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
+      *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
+    }
   };
 
   // ---- online softmax state (one query per lane; both lane halves agree) ----
@@ -669,13 +737,14 @@ prefill_kernel(PrefillArgs a) {
     // an iteration ahead of group B (waves 4-7); each SIMD hosts one wave of
     // each group, so in every phase one of them issues MFMAs while the other
     // runs the softmax.  Tile i lives in stage i % 3.
-    //   phase Y_i:   A PV(i), QK(i+1)      | B softmax(i); all: store tile i+2
-    //   phase X_i+1: A softmax(i+1)        | B PV(i), QK(i+1)
+    //   phase Y_i:   A PV(i), QK(i+1)      | B softmax(i)
+    //   phase X_i+1: A softmax(i+1)        | B PV(i), QK(i+1); both store
+    //                their part of tile i+2
     // Stage (i+2) % 3 == (i-1) % 3 is last read by B in phase X_i.  Each
     // group runs one PV+QK stream per iteration; the QK of the last one reads
     // a stage no one writes any more and its scores are never used.
-    //   Tile i + 4 is fetched into registers in phase Y_i and stored in
-    // Y_i+2: two register sets, the loop unrolled by two so each is fixed.
+    //   Tile i + 4 is fetched into registers in phase X_i+1 and stored in
+    // X_i+3: two register sets, the loop unrolled by two so each is fixed.
     // Past the end of the list the loads read zeros (no memory traffic) and
     // the stores fill a stage no one reads, so the loop body has no branches
     // around its memory operations.
@@ -684,22 +753,38 @@ prefill_kernel(PrefillArgs a) {
       Staged sg0, sg1;
       int kt[5];  // tiles i .. i+4
       tiles_or_none(0, kt);
-      load_tile(kt[0], sg0);
-      load_tile(kt[1], sg1);
-      q_from_lds();
-      store_tile(stage(0), sg0);
-      store_tile(stage(1), sg1);
-      load_tile(kt[2], sg0);
-      load_tile(kt[3], sg1);
-      // the page bases of tile i + 4, read outside the MFMA streams
       PageBases pt4{};
-      if constexpr (PAGED) pt4 = paged_tile(kt[4]);
-      __syncthreads();
-      // Each group runs its own copy of the loop (same barriers in the same
-      // order), so that the compiler sees one group's loads and stores as
-      // straight-line code and waits for exactly the older register set.
+      // Each group runs its own copy of the prologue and the loop (same
+      // barriers in the same order), so that the compiler sees one group's
+      // loads and stores as straight-line code and waits for exactly the
+      // older register set.
       auto run = [&](auto is_a) INLINE {
         constexpr bool A = decltype(is_a)::value;
+        auto pp_load = [&](int t, Staged& sg) INLINE {
+          PageBases pt{};
+          if constexpr (PAGED) pt = paged_tile(t);
+          if constexpr (A) load_v_a(t, pt, sg);
+          else load_k_b(t, pt, sg);
+        };
+        auto pp_store = [&](bf16_t* stg, const Staged& sg) INLINE {
+          if constexpr (A) {
+#pragma unroll
+            for (int i = 0; i < VU_A; ++i) store_v_a(stg, sg, i);
+          } else {
+#pragma unroll
+            for (int i = 0; i < KC_B; ++i) store_k_b(stg, sg, i);
+          }
+        };
+        pp_load(kt[0], sg0);
+        pp_load(kt[1], sg1);
+        q_from_lds();
+        pp_store(stage(0), sg0);
+        pp_store(stage(1), sg1);
+        pp_load(kt[2], sg0);
+        pp_load(kt[3], sg1);
+        // the page bases of tile i + 4, read outside the MFMA streams
+        if constexpr (PAGED) pt4 = paged_tile(kt[4]);
+        __syncthreads();
         // phase X_0 (A starts half an iteration ahead with QK(0))
         if (A) stream(NO, YES, 0, 0, no_hook);
         __syncthreads();
@@ -714,21 +799,28 @@ prefill_kernel(PrefillArgs a) {
           const int slot2 = slot1 == 2 ? 0 : slot1 + 1; // (i + 2) % 3 == (i - 1) % 3
           bf16_t* const dst = stage(slot2);
           const int kt_load = kt[4];
-          // The group stages its own part of tile i + 2 (into the stage no one
-          // reads in either phase) and fetches its part of tile i + 4: the K
-          // chunks between the MFMAs of its stream, where its LDS and memory
-          // ports are otherwise idle, and the V units (transposed on the way,
-          // VALU work) in its softmax phase, which is the shorter one.
+          // Each group stages its part of tile i + 2 (into the stage no one
+          // reads in either phase) and fetches that part of tile i + 4: B the
+          // K chunks, between the MFMAs of its stream, where its LDS and
+          // memory ports are otherwise idle; A the V units (transposed on the
+          // way, VALU work) in its softmax phase.  B's waves are the younger
+          // ones and lose the issue arbitration, so its phases run longer:
+          // leaving it no VALU staging balances them (each group staging half
+          // of both parts was 2.4-3.2 % slower).
           auto stage_hook = [&](auto jc) INLINE {
             constexpr int j = decltype(jc)::value;
-            constexpr int K0 = 2, L0 = K0 + 2 * KC_PER_T;
-            if constexpr (j >= K0 && j < L0 && (j - K0) % 2 == 0) store_k(dst, sg, (j - K0) / 2);
-            if constexpr (j == L0) load_part_pt(kt_load, pt4, sg, K_PART);
+            constexpr int K0 = 2, L0 = K0 + 2 * KC_B;
+            if constexpr (!A) {
+              if constexpr (j >= K0 && j < L0 && (j - K0) % 2 == 0) store_k_b(dst, sg, (j - K0) / 2);
+              if constexpr (j == L0) load_k_b(kt_load, pt4, sg);
+            }
           };
           auto softmax_v = [&](int kt_s) INLINE {
+            if constexpr (A) {
 #pragma unroll
-            for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
-            load_part_pt(kt_load, pt4, sg, V_PART);
+              for (int u = 0; u < VU_A; ++u) store_v_a(dst, sg, u);
+              load_v_a(kt_load, pt4, sg);
+            }
             softmax(kt_s);
           };
           // phase Y_i: A streams PV(i), QK(i+1); B takes the softmax of tile i
@@ -740,8 +832,8 @@ prefill_kernel(PrefillArgs a) {
             stream(YES, YES, slot, slot1, stage_hook);
           } else {
 #pragma unroll
-            for (int u = 0; u < VU_PER_T; ++u) store_v(dst, sg, u);
-            load_part_pt(kt_load, pt4, sg, V_PART);
+            for (int u = 0; u < VU_A; ++u) store_v_a(dst, sg, u);
+            load_v_a(kt_load, pt4, sg);
             if (it + 1 < n_tiles) softmax(kt[1]);
           }
 #pragma unroll
