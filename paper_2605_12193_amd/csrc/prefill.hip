@@ -429,8 +429,32 @@ prefill_kernel(PrefillArgs a) {
       kj_g[i] = ps < TILE ? ((wave_g * 64 + i * GT) / (C / 8)) >> ps_shift : 0;
   }
 
+  // GQA 5: the work item's five waves sit on four SIMDs, waves 0 and 4 on
+  // the same one, which therefore carries twice the MFMA and softmax work.
+  // Only waves 1-3 stage tiles (the same pattern over their 192 threads), so
+  // the doubled SIMD carries no staging.
+  constexpr bool S5 = !PP && HALF && M == 5;
+  constexpr int SNT = 192;
+  constexpr int KC_S = S5 ? (CF::K_CHUNKS + SNT - 1) / SNT : 0, VU_S = S5 ? (CF::V_UNITS + SNT - 1) / SNT : 0;
+  constexpr int K_ROW_STEP_S = SNT / (C / 8), V_CE_STEP_S = SNT / (TILE / 2);
+  const int sidx = tid - 64;   // waves 1-3: 0 .. 191
+  const bool stager = S5 && __builtin_amdgcn_readfirstlane(wave) >= 1 && __builtin_amdgcn_readfirstlane(wave) <= 3;
+  const int k_row_s = sidx / (C / 8), k_ce_s = sidx % (C / 8);
+  const uint32_t k_boff_s = (uint32_t)(((int64_t)k_row_s * st + 8 * k_ce_s) * 2);
+  const uint32_t k_step_s = (uint32_t)(K_ROW_STEP_S * st * 2);
+  const int v_ce_s = sidx / (TILE / 2);
+  const uint32_t v_boff_s = (uint32_t)(((int64_t)(2 * v_j) * st + 8 * v_ce_s) * 2);
+  constexpr uint32_t V_STEP_S = V_CE_STEP_S * 8 * 2;
+  int kj_s[KC_S > 0 ? KC_S : 1];
+  {
+    const int wave_s = __builtin_amdgcn_readfirstlane(wave) - 1;
+#pragma unroll
+    for (int i = 0; i < KC_S; ++i)
+      kj_s[i] = ps < TILE ? ((wave_s * 64 + i * SNT) / (C / 8)) >> ps_shift : 0;
+  }
   // one K/V tile on its way from memory to LDS, in registers
-  constexpr int KS = KC_PER_T > KC_B ? KC_PER_T : KC_B, VS = VU_PER_T > VU_A ? VU_PER_T : VU_A;
+  constexpr int KS0 = KC_PER_T > KC_B ? KC_PER_T : KC_B, VS0 = VU_PER_T > VU_A ? VU_PER_T : VU_A;
+  constexpr int KS = KS0 > KC_S ? KS0 : KC_S, VS = VS0 > VU_S ? VS0 : VU_S;
   struct Staged {
     uint4 k[KS];
     uint4 v[VS][2];
@@ -497,6 +521,21 @@ prefill_kernel(PrefillArgs a) {
   const std::integral_constant<int, 3> KV_PARTS;
   auto load_tile = [&](int kt, Staged& sg) INLINE { load_part(kt, sg, KV_PARTS); };
 
+  // One V unit (keys 2 v_j, 2 v_j + 1 x channels 8 ce .. 8 ce + 7) written
+  // transposed into the V^T rows of stage stg.
+  auto put_v = [&](bf16_t* stg, const uint4 (&u)[2], int ce) INLINE {
+    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&u[0]);
+    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&u[1]);
+    bf16_t* col = stg + CF::K_ELEMS + 8 * ce * CF::VROW + vperm(2 * v_j);
+#pragma unroll
+    for (int e2 = 0; e2 < 4; ++e2) {
+      // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
+      const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
+      const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
+      *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
+      *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
+    }
+  };
   // The staging stores of one thread, as pieces that can be placed apart:
   // K chunk i, and V unit i (two keys x 8 channels, transposed on the way).
   auto store_k = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
@@ -505,18 +544,7 @@ prefill_kernel(PrefillArgs a) {
   };
   auto store_v = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
     if (CF::V_UNITS % NT == 0 || tid + i * NT < CF::V_UNITS) {
-      const int pos = vperm(2 * v_j);
-      const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
-      const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
-      bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce * CF::VROW + pos + i * 8 * V_CE_STEP * CF::VROW;
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        // channels 8ce + 2e2 (low halves) and 8ce + 2e2 + 1 (high halves)
-        const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
-        const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
-        *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
-        *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
-      }
+      put_v(stg, sg.v[i], v_ce + i * V_CE_STEP);
     }
   };
   auto store_tile = [&](bf16_t* stg, const Staged& sg) INLINE {
@@ -558,17 +586,7 @@ prefill_kernel(PrefillArgs a) {
     *reinterpret_cast<uint4*>(stg + k_row_g * CF::KROW + 8 * k_ce_g + i * K_ROW_STEP_G * CF::KROW) = sg.k[i];
   };
   auto store_v_a = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
-    const int pos = vperm(2 * v_j);
-    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&sg.v[i][0]);
-    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&sg.v[i][1]);
-    bf16_t* col = stg + CF::K_ELEMS + 8 * v_ce_g * CF::VROW + pos + i * 8 * V_CE_STEP_G * CF::VROW;
-#pragma unroll
-    for (int e2 = 0; e2 < 4; ++e2) {
-      const uint32_t lo = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x05040100u);
-      const uint32_t hi2 = __builtin_amdgcn_perm(r1[e2], r0[e2], 0x07060302u);
-      *reinterpret_cast<uint32_t*>(col + (2 * e2) * CF::VROW) = lo;
-      *reinterpret_cast<uint32_t*>(col + (2 * e2 + 1) * CF::VROW) = hi2;
-    }
+    put_v(stg, sg.v[i], v_ce_g + i * V_CE_STEP_G);
   };
 
   // ---- online softmax state (one query per lane; both lane halves agree) ----
@@ -582,6 +600,46 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
+  // GQA 5 staging by waves 1-3: fetch / store K chunk i (i < KC_S) and V
+  // unit i (i < VU_S) of their pattern
+  auto load_s = [&](int kt, Staged& sg) INLINE {
+    PageBases pt{};
+    if constexpr (PAGED) pt = paged_tile(kt);
+    uint32_t kbase[KC_S > 0 ? KC_S : 1];
+    uint32_t b0, b1;
+    if constexpr (PAGED) {
+      const int vb = page_lanes(pt);
+#pragma unroll
+      for (int i = 0; i < KC_S; ++i) kbase[i] = (uint32_t)__builtin_amdgcn_readlane(vb, kj_s[i]);
+      v_pair_bases(pt, vj_hi, vj_lo, 2 * v_j, b0, b1);
+    } else {
+      const uint32_t base = (unsigned)kt < (unsigned)t_kv ? (uint32_t)kt * tile_bytes : 0x80000000u;
+#pragma unroll
+      for (int i = 0; i < KC_S; ++i) kbase[i] = base;
+      b0 = b1 = base;
+    }
+#pragma unroll
+    for (int i = 0; i < KC_S; ++i)
+      if (CF::K_CHUNKS % SNT == 0 || sidx + i * SNT < CF::K_CHUNKS)
+        sg.k[i] = bload16(krs, (kbase[i] + i * k_step_s) + k_boff_s);
+    b0 += v_boff_s;
+    b1 += v_boff_s + st_bytes;
+#pragma unroll
+    for (int i = 0; i < VU_S; ++i)
+      if (CF::V_UNITS % SNT == 0 || sidx + i * SNT < CF::V_UNITS) {
+        sg.v[i][0] = bload16(vrs, b0 + i * V_STEP_S);
+        sg.v[i][1] = bload16(vrs, b1 + i * V_STEP_S);
+      }
+  };
+  auto store_k_s = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    if (CF::K_CHUNKS % SNT == 0 || sidx + i * SNT < CF::K_CHUNKS)
+      *reinterpret_cast<uint4*>(stg + k_row_s * CF::KROW + 8 * k_ce_s + i * K_ROW_STEP_S * CF::KROW) = sg.k[i];
+  };
+  auto store_v_s = [&](bf16_t* stg, const Staged& sg, int i) INLINE {
+    if (CF::V_UNITS % SNT == 0 || sidx + i * SNT < CF::V_UNITS) {
+      put_v(stg, sg.v[i], v_ce_s + i * V_CE_STEP_S);
+    }
+  };
   // (the index is made explicitly uniform: inside the unrolled ping-pong loop
   // the compiler no longer proves it so and would emit a vector load)
   auto tile_at = [&](int i) INLINE -> int {
@@ -866,16 +924,31 @@ prefill_kernel(PrefillArgs a) {
       Staged sg;
       int kt01[2];   // list entries 0 and 1
       tiles_or_none(0, kt01);
-      load_tile(kt01[0], sg);
-      if constexpr (HALF) {
-        // half-tile shapes (GQA 5-8): tile 1 joins the same round trip
+      if constexpr (S5) {
+        Staged sg1;
+        if (stager) {
+          load_s(kt01[0], sg);
+          load_s(kt01[1], sg1);
+        }
+        q_from_lds();
+        if (stager) {
+#pragma unroll
+          for (int i = 0; i < KC_S; ++i) store_k_s(stage(0), sg, i);
+#pragma unroll
+          for (int i = 0; i < VU_S; ++i) store_v_s(stage(0), sg, i);
+        }
+        sg = sg1;
+      } else if constexpr (HALF) {
+        // half-tile shapes (GQA 6-8): tile 1 joins the same round trip
         // (measured faster there, slower for the 2-wave GQA 1 shape)
         Staged sg1;
+        load_tile(kt01[0], sg);
         load_tile(kt01[1], sg1);
         q_from_lds();
         store_tile(stage(0), sg);
         sg = sg1;
       } else {
+        load_tile(kt01[0], sg);
         q_from_lds();   // overlaps the first tile's round trip
         store_tile(stage(0), sg);
         load_tile(kt01[1], sg);
@@ -889,11 +962,19 @@ prefill_kernel(PrefillArgs a) {
         const int kt_load = tile_or_none(it + 2);
         auto stage_hook = [&](auto jc) INLINE {
           constexpr int j = decltype(jc)::value;
-          constexpr int K0 = 1, V0 = K0 + KC_PER_T, L0 = V0 + VU_PER_T;
-          static_assert(L0 < 4 * NCB, "staging pieces must fit the PV stream");
-          if constexpr (j >= K0 && j < V0) store_k(dst, sg, j - K0);
-          if constexpr (j >= V0 && j < L0) store_v(dst, sg, j - V0);
-          if constexpr (j == L0) load_tile(kt_load, sg);
+          if constexpr (S5) {
+            constexpr int K0 = 1, V0 = K0 + KC_S, L0 = V0 + VU_S;
+            static_assert(L0 < 4 * NCB, "staging pieces must fit the PV stream");
+            if constexpr (j >= K0 && j < V0) { if (stager) store_k_s(dst, sg, j - K0); }
+            if constexpr (j >= V0 && j < L0) { if (stager) store_v_s(dst, sg, j - V0); }
+            if constexpr (j == L0) { if (stager) load_s(kt_load, sg); }
+          } else {
+            constexpr int K0 = 1, V0 = K0 + KC_PER_T, L0 = V0 + VU_PER_T;
+            static_assert(L0 < 4 * NCB, "staging pieces must fit the PV stream");
+            if constexpr (j >= K0 && j < V0) store_k(dst, sg, j - K0);
+            if constexpr (j >= V0 && j < L0) store_v(dst, sg, j - V0);
+            if constexpr (j == L0) load_tile(kt_load, sg);
+          }
         };
         stream(NO, YES, 0, it & 1, no_hook);
         softmax(kt_cur);
