@@ -429,16 +429,20 @@ prefill_kernel(PrefillArgs a) {
       kj_g[i] = ps < TILE ? ((wave_g * 64 + i * GT) / (C / 8)) >> ps_shift : 0;
   }
 
-  // GQA 5: the work item's five waves sit on four SIMDs, waves 0 and 4 on
-  // the same one, which therefore carries twice the MFMA and softmax work.
-  // Only waves 1-3 stage tiles (the same pattern over their 192 threads), so
-  // the doubled SIMD carries no staging.
-  constexpr bool S5 = !PP && HALF && M == 5;
-  constexpr int SNT = 192;
-  constexpr int KC_S = S5 ? (CF::K_CHUNKS + SNT - 1) / SNT : 0, VU_S = S5 ? (CF::V_UNITS + SNT - 1) / SNT : 0;
+  // GQA 5 and 6: the work item's waves sit on four SIMDs, waves w and w + 4
+  // on the same one (w = 0, and 1 at GQA 6), which therefore carries twice
+  // the MFMA and softmax work.  Only the waves alone on their SIMD (1-3, or
+  // 2-3) stage tiles, with the same pattern over their threads, so the
+  // doubled SIMDs carry no staging.  (At GQA 7 one wave would stage a whole
+  // tile: 128 VGPRs of staging registers.)
+  constexpr bool SOLO = !PP && HALF && (M == 5 || M == 6);
+  constexpr int SW0 = M == 5 ? 1 : 2;   // first staging wave
+  constexpr int SNT = (4 - SW0) * 64;
+  constexpr int KC_S = SOLO ? (CF::K_CHUNKS + SNT - 1) / SNT : 0, VU_S = SOLO ? (CF::V_UNITS + SNT - 1) / SNT : 0;
   constexpr int K_ROW_STEP_S = SNT / (C / 8), V_CE_STEP_S = SNT / (TILE / 2);
-  const int sidx = tid - 64;   // waves 1-3: 0 .. 191
-  const bool stager = S5 && __builtin_amdgcn_readfirstlane(wave) >= 1 && __builtin_amdgcn_readfirstlane(wave) <= 3;
+  const int sidx = tid - 64 * SW0;   // 0 .. SNT - 1 on the staging waves
+  const bool stager = SOLO && __builtin_amdgcn_readfirstlane(wave) >= SW0 &&
+                      __builtin_amdgcn_readfirstlane(wave) <= 3;
   const int k_row_s = sidx / (C / 8), k_ce_s = sidx % (C / 8);
   const uint32_t k_boff_s = (uint32_t)(((int64_t)k_row_s * st + 8 * k_ce_s) * 2);
   const uint32_t k_step_s = (uint32_t)(K_ROW_STEP_S * st * 2);
@@ -447,7 +451,7 @@ prefill_kernel(PrefillArgs a) {
   constexpr uint32_t V_STEP_S = V_CE_STEP_S * 8 * 2;
   int kj_s[KC_S > 0 ? KC_S : 1];
   {
-    const int wave_s = __builtin_amdgcn_readfirstlane(wave) - 1;
+    const int wave_s = __builtin_amdgcn_readfirstlane(wave) - SW0;
 #pragma unroll
     for (int i = 0; i < KC_S; ++i)
       kj_s[i] = ps < TILE ? ((wave_s * 64 + i * SNT) / (C / 8)) >> ps_shift : 0;
@@ -600,8 +604,8 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
-  // GQA 5 staging by waves 1-3: fetch / store K chunk i (i < KC_S) and V
-  // unit i (i < VU_S) of their pattern
+  // GQA 5 and 6 staging by the waves alone on their SIMD: fetch / store K
+  // chunk i (i < KC_S) and V unit i (i < VU_S) of their pattern
   auto load_s = [&](int kt, Staged& sg) INLINE {
     PageBases pt{};
     if constexpr (PAGED) pt = paged_tile(kt);
@@ -924,7 +928,7 @@ prefill_kernel(PrefillArgs a) {
       Staged sg;
       int kt01[2];   // list entries 0 and 1
       tiles_or_none(0, kt01);
-      if constexpr (S5) {
+      if constexpr (SOLO) {
         Staged sg1;
         if (stager) {
           load_s(kt01[0], sg);
@@ -962,7 +966,7 @@ prefill_kernel(PrefillArgs a) {
         const int kt_load = tile_or_none(it + 2);
         auto stage_hook = [&](auto jc) INLINE {
           constexpr int j = decltype(jc)::value;
-          if constexpr (S5) {
+          if constexpr (SOLO) {
             constexpr int K0 = 1, V0 = K0 + KC_S, L0 = V0 + VU_S;
             static_assert(L0 < 4 * NCB, "staging pieces must fit the PV stream");
             if constexpr (j >= K0 && j < V0) { if (stager) store_k_s(dst, sg, j - K0); }
