@@ -429,14 +429,14 @@ prefill_kernel(PrefillArgs a) {
       kj_g[i] = ps < TILE ? ((wave_g * 64 + i * GT) / (C / 8)) >> ps_shift : 0;
   }
 
-  // GQA 5 and 6: the work item's waves sit on four SIMDs, waves w and w + 4
-  // on the same one (w = 0, and 1 at GQA 6), which therefore carries twice
-  // the MFMA and softmax work.  Only the waves alone on their SIMD (1-3, or
-  // 2-3) stage tiles, with the same pattern over their threads, so the
-  // doubled SIMDs carry no staging.  (At GQA 7 one wave would stage a whole
-  // tile: 128 VGPRs of staging registers.)
-  constexpr bool SOLO = !PP && HALF && (M == 5 || M == 6);
-  constexpr int SW0 = M == 5 ? 1 : 2;   // first staging wave
+  // Five- and six-wave work items (GQA 5; GQA 3 and 6): the waves sit on
+  // four SIMDs, waves w and w + 4 on the same one (w = 0, and 1 with six
+  // waves), which therefore carries twice the MFMA and softmax work.  Only
+  // the waves alone on their SIMD (1-3, or 2-3) stage tiles, with the same
+  // pattern over their threads, so the doubled SIMDs carry no staging.  (With
+  // seven waves one wave would stage a whole tile: 128 VGPRs of staging.)
+  constexpr bool SOLO = !PP && (Shape<C, M>::WAVES == 5 || Shape<C, M>::WAVES == 6);
+  constexpr int SW0 = Shape<C, M>::WAVES - 4;   // first staging wave
   constexpr int SNT = (4 - SW0) * 64;
   constexpr int KC_S = SOLO ? (CF::K_CHUNKS + SNT - 1) / SNT : 0, VU_S = SOLO ? (CF::V_UNITS + SNT - 1) / SNT : 0;
   constexpr int K_ROW_STEP_S = SNT / (C / 8), V_CE_STEP_S = SNT / (TILE / 2);
@@ -604,8 +604,8 @@ prefill_kernel(PrefillArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[cb][r] = 0.f;
 
-  // GQA 5 and 6 staging by the waves alone on their SIMD: fetch / store K
-  // chunk i (i < KC_S) and V unit i (i < VU_S) of their pattern
+  // Staging by the waves alone on their SIMD (five and six waves): fetch /
+  // store K chunk i (i < KC_S) and V unit i (i < VU_S) of their pattern
   auto load_s = [&](int kt, Staged& sg) INLINE {
     PageBases pt{};
     if constexpr (PAGED) pt = paged_tile(kt);
